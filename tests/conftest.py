@@ -1,0 +1,29 @@
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+
+def pytest_configure(config):
+    config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
+    config.addinivalue_line("markers", "slow: long-running CPU oracle work")
+
+
+_WEIGHTS = {}
+
+
+@pytest.fixture(scope="session")
+def weights_cache():
+    """Session cache of generated weights keyed by workload name."""
+    from fixtures import make_weights
+
+    def get(workload):
+        if workload not in _WEIGHTS:
+            _WEIGHTS[workload] = make_weights(workload)
+        return _WEIGHTS[workload]
+
+    return get
