@@ -1,0 +1,167 @@
+"""Benchmark of the step-level continuous-batching UNet step on one MI355X.
+
+Workload: SD-1.5-shaped UNet (latent 4x64x64, channels 320/640/1280/1280),
+bf16, a continuous batch of 32 requests at seeded timesteps in [0, 999],
+half of them under Skip-CFG (48 packed rows), per-request guidance in [5, 9]
+and text contexts, one UNet evaluation + CFG combine + DDIM update per step.
+Random-init weights and synthetic inputs (the step's cost is independent of
+the values).
+
+Prints ONE JSON line: rows*steps/s (value), the fraction of the bf16 MFMA
+peak the whole step reaches, the roofline of the dominant kernel class
+(the MFMA implicit-GEMM convolution/linear kernel) measured with HIP events
+on the launch stream, and the CPU oracle timed on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+WORKLOAD = "c3_sd15_mixed32"
+METRIC = "UNet rows·steps/sec + % bf16 MFMA peak, SD-1.5-shape, 32-req mixed-CFG batch"
+PEAK_BF16 = 2.5166e15  # dense bf16 MFMA, 256 CU x 4096 FLOP/clk x 2.4 GHz
+PEAK_HBM = 8.0e12
+FLOP_PER_ROW = 803.27e9  # algorithmic FLOPs of one SD-1.5 UNet evaluation at 64x64
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(unet, weights, req, budget_s=25.0):
+    """The oracle, as it is, on a bounded sample: whole requests (one
+    Skip-CFG request = 1 row, one CFG request = 2 rows) until ~budget_s."""
+    import oracle
+    from oracle.unet import Weights
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count()
+    W = Weights(weights)
+    for name in weights:  # one-off fp64 conversion of the parameters (setup)
+        W(name)
+    order = list(np.flatnonzero(req["cfg_on"] == 0)) + list(np.flatnonzero(req["cfg_on"] == 1))
+    rows, t0 = 0, time.perf_counter()
+    done = []
+    for r in order:
+        oracle.unet_step(unet, W, req, only=[int(r)])
+        rows += 1 + int(req["cfg_on"][r])
+        done.append(int(r))
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    el = time.perf_counter() - t0
+    return {"value": rows / el, "unit": "rows·steps/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{len(done)} requests ({rows} UNet rows) of the same 32-request batch, "
+                      f"one full float64 step each, {el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the step shards by request with no collective, "
+              f"and this build runs on a single MI355X (got --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from fixtures import get_config, make_requests, make_weights
+    from paper_2605_08835_amd import UNet
+
+    spec = get_config(WORKLOAD)
+    unet = spec["unet"]
+    t0 = time.time()
+    weights = make_weights(WORKLOAD)
+    req = make_requests(WORKLOAD)
+    log(f"inputs ready in {time.time() - t0:.1f} s")
+    R = len(req["timesteps"])
+    rows = int(R + req["cfg_on"].sum())
+    m = UNet(unet, max_requests=R, device="cuda:0")
+    m.load_weights(weights)
+    dev = torch.device("cuda:0")
+    act = m.act_dtype
+    lat = torch.from_numpy(req["latents"]).to(dev)
+    ctx = torch.from_numpy(req["ctx_cond"]).to(dev).to(act)
+    unc = torch.from_numpy(req["ctx_uncond"]).to(dev).to(act)
+    coef = m.coefficients(req["schedule"], req["timesteps"], req["t_prev"])
+    out = torch.empty_like(lat)
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        m.step(lat, req["timesteps"], req["cfg_on"], req["guidance"], ctx, unc, coef, out=out, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    log(f"timed {args.steps} steps: {ms:.3f} ms/step")
+
+    # Per-kernel-class split: the same steps again with an event after every launch.
+    m.profile(True)
+    m.profile_read(reset=True)
+    for _ in range(args.steps):
+        step()
+        m.profile_read(reset=False)
+    prof = m.profile_read(reset=True)
+    m.profile(False)
+    kernels = {}
+    for k, v in prof.items():
+        n = v["launches"]
+        kernels[k] = {"launches_per_step": n / args.steps, "ms_per_step": v["ms"] / args.steps,
+                      "avg_launch_us": 1e3 * v["ms"] / max(n, 1),
+                      "tflops": v["flop"] / max(v["ms"], 1e-9) / 1e9,
+                      "gbps": v["bytes"] / max(v["ms"], 1e-9) / 1e6}
+    g = prof.get("gemm", {"launches": 1, "ms": 1.0, "flop": 0.0, "bytes": 0.0})
+    g_launches = g["launches"] / args.steps
+    flop_per_launch = g["flop"] / max(g["launches"], 1)
+    avg_s = g["ms"] / max(g["launches"], 1) / 1e3
+    achieved = flop_per_launch / avg_s / 1e12
+    roof = {"kernel": "gemm_bf16_kernel (implicit-GEMM conv / linear, MFMA 32x32x16 bf16)",
+            "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
+            "frac": round(achieved * 1e12 / PEAK_BF16, 4), "traffic": None,
+            "flop_per_launch": flop_per_launch, "launches_per_step": g_launches,
+            "avg_launch_us": round(avg_s * 1e6, 2)}
+
+    value = rows * 1e3 / ms
+    res = {
+        "metric": METRIC, "value": round(value, 2), "unit": "rows·steps/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) latents and contexts, random-init N(0,0.02) weights)",
+        "config": {"workload": "SD-1.5-shaped UNet, latent 4x64x64, bf16; 32 requests at seeded "
+                               "timesteps, 16 under Skip-CFG -> 48 packed rows; guidance U[5,9]; "
+                               "77x768 contexts; UNet + CFG combine + DDIM per step",
+                   "requests": R, "rows": rows, "latent": [4, 64, 64]},
+        "requests_steps_per_s": round(R * 1e3 / ms, 2),
+        "pct_bf16_peak": round(100 * value * FLOP_PER_ROW / PEAK_BF16, 2),
+        "roofline": roof,
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample ...")
+        res["cpu_baseline"] = cpu_baseline(unet, weights, req)
+    m.close()
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,76 @@
+/*
+ * synerdiff_ops.h - kernel-level entry points of the UNet step.
+ *
+ * Each call runs one of the step's kernels on caller-owned device buffers so
+ * that a kernel can be checked on its own against the layer it implements.
+ * Conventions as in synerdiff.h: device pointers, the caller's stream,
+ * validation before enqueue, SD_ERR_HIP on a launch failure.  `dtype` is
+ * SD_F32 or SD_BF16 and types every activation and weight argument; norm
+ * statistics, biases and affine parameters are always fp32.
+ * Activations are channels-last: [n, H, W, C].
+ */
+#ifndef SYNERDIFF_OPS_H
+#define SYNERDIFF_OPS_H
+
+#include "synerdiff.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Convolution as an implicit GEMM (3x3 or 1x1 layers of the UNet):
+ *   out[i, y, x, o] = bias[o] + resid[i, y, x, o]
+ *       + sum_{ky, kx, c} A(i, s*y + ky - p, s*x + kx - p, c) * w[o, (ky*ks + kx)*cin + c]
+ * with p = (ks - 1) / 2, cin = c0 + c1, A the channel concat [x0 | x1]
+ * (x1 may be NULL with c1 = 0), optionally nearest-2x upsampled first
+ * (up = 1), optionally transformed per (image, channel) as
+ * v * scale + shift (GroupNorm affine; scale/shift [n, cin] fp32 or NULL)
+ * and then SiLU (silu = 1), and zero outside the image (zero padding after
+ * the transform).  Output size: H/stride (stride 2 needs even H, W) or 2H
+ * when upsampling.  w is the packed weight [cout, ks*ks*cin] (tap-major,
+ * channel-minor).  bias may be NULL; resid ([n, Ho, Wo, cout], activation
+ * dtype) may be NULL or equal to out.  out_f32 = 1 writes fp32 output.
+ * Constraints: ks in {1, 3}; stride in {1, 2}; c0, c1 multiples of 8. */
+sd_status synerdiff_op_conv(int32_t dtype, const void* d_x0, int32_t c0, const void* d_x1, int32_t c1,
+                            int32_t n, int32_t H, int32_t W, int32_t ks, int32_t stride, int32_t up,
+                            const float* d_scale, const float* d_shift, int32_t silu, const void* d_w,
+                            int32_t cout, const float* d_bias, const void* d_resid, void* d_out,
+                            int32_t out_f32, void* hip_stream);
+
+/* Multi-head attention O = softmax(Q K^T * scale) V per image and head
+ * (head h uses columns [h*d, (h+1)*d) of each token's row).  Q: image i,
+ * token t at q + i*q_img + t*q_ld; K and V likewise with kv_img, kv_ld and
+ * image kv_index[i] (d_kv_index NULL = image i); O like Q with o_img, o_ld.
+ * Strides in elements.  Constraints: d a multiple of 8; bf16: d <= 256 and
+ * not in (192, 224]; fp32: d <= 64. */
+sd_status synerdiff_op_attention(int32_t dtype, const void* d_q, int64_t q_ld, int64_t q_img,
+                                 const void* d_k, const void* d_v, int64_t kv_ld, int64_t kv_img,
+                                 const int32_t* d_kv_index, void* d_o, int64_t o_ld, int64_t o_img,
+                                 int32_t n, int32_t heads, int32_t d, int32_t n_q, int32_t n_k,
+                                 float scale, void* hip_stream);
+
+/* GroupNorm statistics of the concat [x0 | x1] ([n, hw, c0 + c1]) with
+ * `groups` groups of consecutive channels, biased variance, eps: writes the
+ * per-(image, channel) affine scale = gamma * rstd, shift = beta - mean *
+ * scale (fp32 [n, cin]) that synerdiff_op_conv applies.  d_partial is
+ * scratch of synerdiff_op_groupnorm_scratch_floats(n, hw, cin) floats. */
+size_t synerdiff_op_groupnorm_scratch_floats(int32_t n, int32_t hw, int32_t cin);
+sd_status synerdiff_op_groupnorm_stats(int32_t dtype, const void* d_x0, int32_t c0, const void* d_x1,
+                                       int32_t c1, int32_t n, int32_t hw, int32_t groups, float eps,
+                                       const float* d_gamma, const float* d_beta, float* d_partial,
+                                       float* d_scale, float* d_shift, void* hip_stream);
+
+/* LayerNorm over the last axis of x [tokens, C] (biased variance):
+ * y = (x - mean) * rstd * gamma + beta.  C a multiple of 8, <= 2048. */
+sd_status synerdiff_op_layernorm(int32_t dtype, const void* d_x, void* d_y, int64_t tokens, int32_t C,
+                                 const float* d_gamma, const float* d_beta, float eps, void* hip_stream);
+
+/* GEGLU: y[t, j] = x[t, j] * GELU(x[t, half + j]) with exact GELU; x is
+ * [tokens, 2*half], y [tokens, half]; half a multiple of 8. */
+sd_status synerdiff_op_geglu(int32_t dtype, const void* d_x, void* d_y, int64_t tokens, int32_t half,
+                             void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SYNERDIFF_OPS_H */

@@ -50,28 +50,34 @@ def cfg_combine(eps_c, eps_u, w):
 
 
 def unet_step_request(cfg, W, x, t, t_prev, cfg_on, w, ctx, ctx_null, abar,
-                      pooled=None, pooled_null=None, time_ids=None, want_eps=False):
+                      pooled=None, pooled_null=None, time_ids=None, want_eps=False, parts=None):
     """One request's step: returns x' (and the guided eps when asked).
 
     With CFG on both the conditional and the unconditional UNet evaluations
     run and are combined; with Skip-CFG only the conditional one runs and its
-    output is used as is (the unconditional branch is bypassed, Sec. III-B)."""
+    output is used as is (the unconditional branch is bypassed, Sec. III-B).
+    When `parts` is a dict it receives the raw branch outputs under "eps_c"
+    and "eps_u" (None under Skip-CFG)."""
     eps_c = unet_eps(cfg, W, x, t, ctx, pooled, time_ids)
+    eps_u = None
     if cfg_on:
         eps_u = unet_eps(cfg, W, x, t, ctx_null, pooled_null, time_ids)
         eps = cfg_combine(eps_c, eps_u, F(w))
     else:
         eps = eps_c
+    if parts is not None:
+        parts["eps_c"], parts["eps_u"] = eps_c, eps_u
     xn = ddim_step(x, eps, abar_at(abar, t), abar_at(abar, t_prev))
     return (xn, eps) if want_eps else xn
 
 
-def unet_step(cfg, weights, req, only=None, want_eps=False):
+def unet_step(cfg, weights, req, only=None, want_eps=False, parts=None):
     """The step over a batch, request by request.  `req` holds latents
     (R, C, H, W), timesteps, t_prev, cfg_on, guidance, ctx_cond (R, L, D),
     ctx_uncond (L, D), schedule and, for SDXL-like configs, pooled_cond,
     pooled_uncond and time_ids.  `only` restricts the work to some requests.
-    Returns {request index: x'} (and {index: eps} when want_eps)."""
+    Returns {request index: x'} (and {index: eps} when want_eps); a dict
+    passed as `parts` receives {index: {"eps_c": ..., "eps_u": ...}}."""
     W = weights if isinstance(weights, Weights) else Weights(weights)
     abar = alphas_cumprod(betas(req["schedule"]))
     idx = range(len(req["timesteps"])) if only is None else only
@@ -81,9 +87,12 @@ def unet_step(cfg, weights, req, only=None, want_eps=False):
         if cfg["add_in"]:
             extra = dict(pooled=req["pooled_cond"][r], pooled_null=req["pooled_uncond"],
                          time_ids=req["time_ids"])
+        p = {} if parts is not None else None
         xn, eps = unet_step_request(
             cfg, W, req["latents"][r], int(req["timesteps"][r]), int(req["t_prev"][r]),
             bool(req["cfg_on"][r]), float(req["guidance"][r]), req["ctx_cond"][r],
-            req["ctx_uncond"], abar, want_eps=True, **extra)
+            req["ctx_uncond"], abar, want_eps=True, parts=p, **extra)
+        if parts is not None:
+            parts[r] = p
         outs[r], epss[r] = xn, eps
     return (outs, epss) if want_eps else outs

@@ -1,0 +1,244 @@
+"""ctypes binding of the synerdiff C ABI (argument marshalling only).
+
+Device buffers are torch tensors on the current HIP device; streams are
+torch streams.  Every computation runs in libsynerdiff.so.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsynerdiff.so")
+_LIB = None
+
+SD_F32, SD_BF16 = 0, 1
+SCHEDULES = {"linear": 0, "scaled_linear": 1}
+STATUS = {0: "SD_OK", -1: "SD_ERR_INVALID_ARG", -2: "SD_ERR_UNSUPPORTED", -3: "SD_ERR_CAPACITY",
+          -4: "SD_ERR_WORKSPACE", -5: "SD_ERR_HIP"}
+
+
+class SynerDiffError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class UNetConfig(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("latent_c", "latent_h", "latent_w", "n_levels")] + \
+               [("ch", ctypes.c_int32 * 4), ("n_res", ctypes.c_int32), ("tx_depth", ctypes.c_int32 * 4)] + \
+               [(n, ctypes.c_int32) for n in ("mid_tx_depth", "heads", "head_dim", "gn_groups", "ctx_len",
+                                               "ctx_dim", "temb_in", "temb_dim", "add_in", "pooled_dim",
+                                               "time_id_dim", "n_time_ids", "max_requests", "dtype")]
+
+
+class KernelStat(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 24), ("launches", ctypes.c_int64), ("ms", ctypes.c_double),
+                ("flop", ctypes.c_double), ("bytes", ctypes.c_double)]
+
+
+_P = ctypes.c_void_p
+_SIG = {
+    "synerdiff_abi_version": (ctypes.c_int32, []),
+    "synerdiff_last_error": (ctypes.c_char_p, []),
+    "synerdiff_config_check": (ctypes.c_int, [ctypes.POINTER(UNetConfig)]),
+    "synerdiff_param_count": (ctypes.c_int64, [ctypes.POINTER(UNetConfig)]),
+    "synerdiff_param_info": (ctypes.c_int, [ctypes.POINTER(UNetConfig), ctypes.c_int64, ctypes.c_char_p,
+                                            ctypes.c_size_t, ctypes.POINTER(ctypes.c_int64),
+                                            ctypes.POINTER(ctypes.c_int32)]),
+    "synerdiff_weights_bytes": (ctypes.c_size_t, [ctypes.POINTER(UNetConfig)]),
+    "synerdiff_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(UNetConfig)]),
+    "synerdiff_unet_create": (ctypes.c_int, [ctypes.POINTER(UNetConfig), _P, ctypes.c_size_t, _P,
+                                             ctypes.c_size_t, ctypes.POINTER(_P)]),
+    "synerdiff_load_weights": (ctypes.c_int, [_P, _P, ctypes.c_size_t, _P]),
+    "synerdiff_unet_step": (ctypes.c_int, [_P, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                           _P, _P]),
+    "synerdiff_row_plan": (ctypes.c_int, [ctypes.c_int32, _P, _P, _P, _P, _P]),
+    "synerdiff_alphas_cumprod": (ctypes.c_int, [ctypes.c_int32, _P]),
+    "synerdiff_ddim_coef": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _P]),
+    "synerdiff_unet_destroy": (None, [_P]),
+    "synerdiff_profile": (ctypes.c_int, [_P, ctypes.c_int32]),
+    "synerdiff_profile_read": (ctypes.c_int, [_P, ctypes.POINTER(KernelStat), ctypes.c_int32,
+                                              ctypes.POINTER(ctypes.c_int32), ctypes.c_int32]),
+    "synerdiff_op_conv": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, _P] + [ctypes.c_int32] * 7 +
+                          [_P, _P, ctypes.c_int32, _P, ctypes.c_int32, _P, _P, _P, ctypes.c_int32, _P]),
+    "synerdiff_op_attention": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int64, ctypes.c_int64, _P, _P,
+                                              ctypes.c_int64, ctypes.c_int64, _P, _P, ctypes.c_int64,
+                                              ctypes.c_int64] + [ctypes.c_int32] * 5 + [ctypes.c_float, _P]),
+    "synerdiff_op_groupnorm_scratch_floats": (ctypes.c_size_t, [ctypes.c_int32] * 3),
+    "synerdiff_op_groupnorm_stats": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, _P] + [ctypes.c_int32] * 4 +
+                                     [ctypes.c_float, _P, _P, _P, _P, _P, _P]),
+    "synerdiff_op_layernorm": (ctypes.c_int, [ctypes.c_int32, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P,
+                                              ctypes.c_float, _P]),
+    "synerdiff_op_geglu": (ctypes.c_int, [ctypes.c_int32, _P, _P, ctypes.c_int64, ctypes.c_int32, _P]),
+}
+
+
+def lib():
+    """The loaded HIP library; raises if it has not been built."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with python -m paper_2605_08835_amd.build")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIG.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _LIB = L
+    return _LIB
+
+
+def _check(status):
+    if status != 0:
+        raise SynerDiffError(status, lib().synerdiff_last_error().decode())
+
+
+def _ptr(a):
+    """Data pointer of a numpy array or torch tensor (None -> NULL)."""
+    if a is None:
+        return None
+    if isinstance(a, np.ndarray):
+        return a.ctypes.data
+    return a.data_ptr()
+
+
+def config_from_dict(unet, max_requests):
+    c = UNetConfig()
+    c.latent_c, c.latent_h, c.latent_w = unet["latent_c"], unet["latent_h"], unet["latent_w"]
+    c.n_levels = len(unet["ch"])
+    for i, v in enumerate(unet["ch"]):
+        c.ch[i] = v
+    for i, v in enumerate(unet["tx_depth"]):
+        c.tx_depth[i] = v
+    c.n_res, c.mid_tx_depth = unet["n_res"], unet["mid_tx_depth"]
+    c.heads, c.head_dim, c.gn_groups = unet["heads"], unet["head_dim"], unet["gn_groups"]
+    c.ctx_len, c.ctx_dim = unet["ctx_len"], unet["ctx_dim"]
+    c.temb_in, c.temb_dim, c.add_in = unet["temb_in"], unet["temb_dim"], unet["add_in"]
+    c.pooled_dim, c.time_id_dim, c.n_time_ids = unet["pooled_dim"], unet["time_id_dim"], unet["n_time_ids"]
+    c.max_requests = max_requests
+    c.dtype = SD_BF16 if unet["dtype"] == "bf16" else SD_F32
+    return c
+
+
+def manifest(cfg):
+    """[(name, shape)] of the parameters the library expects, in load order."""
+    L = lib()
+    n = L.synerdiff_param_count(ctypes.byref(cfg))
+    if n < 0:
+        raise SynerDiffError(-2, L.synerdiff_last_error().decode())
+    out = []
+    name = ctypes.create_string_buffer(256)
+    shape = (ctypes.c_int64 * 4)()
+    nd = ctypes.c_int32()
+    for i in range(n):
+        _check(L.synerdiff_param_info(ctypes.byref(cfg), i, name, 256, shape, ctypes.byref(nd)))
+        out.append((name.value.decode(), tuple(shape[k] for k in range(nd.value))))
+    return out
+
+
+def row_plan(cfg_on):
+    cfg_on = np.ascontiguousarray(cfg_on, np.uint8)
+    n = len(cfg_on)
+    rr, rb = np.zeros(2 * n, np.int32), np.zeros(2 * n, np.int32)
+    ru, nr = np.zeros(n, np.int32), np.zeros(1, np.int32)
+    _check(lib().synerdiff_row_plan(n, _ptr(cfg_on), _ptr(rr), _ptr(rb), _ptr(ru), _ptr(nr)))
+    k = int(nr[0])
+    return dict(row_req=rr[:k], row_branch=rb[:k], req_row_u=ru, n_rows=k)
+
+
+def alphas_cumprod(schedule):
+    out = np.zeros(1000, np.float64)
+    _check(lib().synerdiff_alphas_cumprod(SCHEDULES[schedule], _ptr(out)))
+    return out
+
+
+def ddim_coef(abar, t, t_prev):
+    abar = np.ascontiguousarray(abar, np.float64)
+    out = np.zeros(2, np.float32)
+    _check(lib().synerdiff_ddim_coef(_ptr(abar), int(t), int(t_prev), _ptr(out)))
+    return float(out[0]), float(out[1])
+
+
+class UNet:
+    """One UNet handle over torch-allocated device buffers."""
+
+    def __init__(self, unet, max_requests, device=None):
+        import torch
+        self.torch = torch
+        self.unet = unet
+        self.cfg = config_from_dict(unet, max_requests)
+        L = lib()
+        _check(L.synerdiff_config_check(ctypes.byref(self.cfg)))
+        self.device = torch.device(device or "cuda")
+        self.act_dtype = torch.bfloat16 if unet["dtype"] == "bf16" else torch.float32
+        wb = L.synerdiff_weights_bytes(ctypes.byref(self.cfg))
+        wsb = L.synerdiff_workspace_bytes(ctypes.byref(self.cfg))
+        self.wbuf = torch.empty(wb + 256, dtype=torch.uint8, device=self.device)
+        self.ws = torch.empty(wsb + 256, dtype=torch.uint8, device=self.device)
+        wp, sp = _align(self.wbuf.data_ptr()), _align(self.ws.data_ptr())
+        h = ctypes.c_void_p()
+        _check(L.synerdiff_unet_create(ctypes.byref(self.cfg), wp, wb, sp, wsb, ctypes.byref(h)))
+        self.h = h
+        self.weights_bytes, self.workspace_bytes = wb, wsb
+        self.schedule_abar = {}
+
+    def load_weights(self, weights):
+        """weights: {name: float32 array}; laid out in the library's manifest order."""
+        man = manifest(self.cfg)
+        flat = np.concatenate([np.ascontiguousarray(weights[n], np.float32).ravel() for n, _ in man])
+        _check(lib().synerdiff_load_weights(self.h, _ptr(flat), flat.size, self._stream()))
+
+    def _stream(self, stream=None):
+        s = stream if stream is not None else self.torch.cuda.current_stream(self.device)
+        return s.cuda_stream
+
+    def coefficients(self, schedule, timesteps, t_prev):
+        if schedule not in self.schedule_abar:
+            self.schedule_abar[schedule] = alphas_cumprod(schedule)
+        ab = self.schedule_abar[schedule]
+        return np.array([ddim_coef(ab, t, tp) for t, tp in zip(timesteps, t_prev)], np.float32)
+
+    def step(self, latents, timesteps, cfg_on, guidance, ctx_cond, ctx_uncond, coef, out=None,
+             eps_out=None, pooled_cond=None, pooled_uncond=None, time_ids=None, stream=None):
+        """Enqueue one step.  latents, ctx_*, pooled_*, out and eps_out are
+        device tensors; timesteps, cfg_on, guidance, coef and time_ids are
+        host arrays.  Returns out."""
+        n = int(latents.shape[0])
+        ts = np.ascontiguousarray(timesteps, np.int32)
+        cf = np.ascontiguousarray(cfg_on, np.uint8)
+        gd = np.ascontiguousarray(guidance, np.float32)
+        cc = np.ascontiguousarray(coef, np.float32).reshape(-1)
+        ti = None if time_ids is None else np.ascontiguousarray(time_ids, np.float32)
+        if out is None:
+            out = self.torch.empty_like(latents)
+        _check(lib().synerdiff_unet_step(self.h, n, _ptr(latents), _ptr(ts), _ptr(cf), _ptr(gd), _ptr(ctx_cond),
+                                         _ptr(ctx_uncond), _ptr(pooled_cond), _ptr(pooled_uncond), _ptr(ti),
+                                         _ptr(cc), _ptr(out), _ptr(eps_out), self._stream(stream)))
+        return out
+
+    def profile(self, enable=True):
+        _check(lib().synerdiff_profile(self.h, int(enable)))
+
+    def profile_read(self, reset=True):
+        """{kernel class: dict(launches, ms, flop, bytes)} since the last reset."""
+        arr = (KernelStat * 16)()
+        n = ctypes.c_int32()
+        _check(lib().synerdiff_profile_read(self.h, arr, 16, ctypes.byref(n), int(reset)))
+        return {arr[i].name.decode(): dict(launches=arr[i].launches, ms=arr[i].ms, flop=arr[i].flop,
+                                           bytes=arr[i].bytes) for i in range(min(n.value, 16))}
+
+    def close(self):
+        if getattr(self, "h", None):
+            lib().synerdiff_unet_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _align(p):
+    return (p + 255) & ~255

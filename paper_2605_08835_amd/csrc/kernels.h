@@ -1,0 +1,106 @@
+// Internal interface between the host runtime and the HIP kernels.
+// Activations are NHWC ("rows" = packed CFG rows = images), stored in the
+// handle's dtype (fp32 or bf16); statistics, biases and accumulators are fp32.
+#pragma once
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace sd {
+
+enum DType { F32 = 0, BF16 = 1 };
+
+// One K-segment of an implicit-GEMM A operand.  Row m of A is output pixel
+// (img, oy, ox) of an Ho x Wo image; column k is (tap, c) with
+// tap = k / cin (ky = tap / ks, kx = tap % ks) and input channel c.  The
+// element is the input pixel under that tap, after the optional nearest-2x
+// upsample, the optional per-(img, channel) affine (GroupNorm) and SiLU, and
+// zero outside the image (conv zero padding).  Channels c < c0 come from
+// src0, the rest from src1 (the skip concat [h | skip] of the up path).
+struct ASeg {
+  const void* src0;
+  const void* src1;
+  const float* scale;  // [imgs, cin] or null
+  const float* shift;  // [imgs, cin]
+  int c0, c1, cin;     // cin = c0 + c1; c0, c1 multiples of 8
+  int ks;              // 1 or 3
+  int stride;          // 1 or 2
+  int up;              // 1: nearest-2x upsample before the conv
+  int Hi, Wi, Ho, Wo;  // input (before upsampling) and output sizes
+  int K;               // ks * ks * cin
+  int silu;
+};
+
+// Epilogue: out[m, n] = acc + bias[n] + tbias[row_req... ] + resid[m, n].
+struct Epi {
+  const float* bias;      // [N] or null
+  const float* tbias;     // time bias: tbias[img * tb_ld + tb_off + n], or null
+  int tb_ld, tb_off, hw;  // img = m / hw
+  const void* resid;      // [M, ldr] in the activation dtype, or null (may equal out)
+  int ldr;
+  void* out;              // [M, ldo]
+  int ldo;
+  int out_f32;            // 1: fp32 output regardless of the activation dtype
+};
+
+struct GemmArgs {
+  int M, N, K;       // K = seg[0].K + seg[1].K (seg[1].K = 0 if unused)
+  ASeg seg[2];
+  const void* B;     // packed weights [N, ldb], K contiguous, activation dtype
+  int ldb;
+  Epi epi;
+};
+
+hipError_t launch_gemm(DType dt, const GemmArgs& a, hipStream_t s);
+
+// Attention: O = softmax(Q K^T * scale) V per (img, head).
+struct AttnArgs {
+  const void* q; long q_ld, q_img;   // token stride, image stride (elements)
+  const void* k; const void* v; long kv_ld, kv_img;
+  const int* kv_index;               // kv image of each q image, or null (= same)
+  void* o; long o_ld, o_img;
+  int imgs, heads, d, Nq, Nk;
+  float scale;
+};
+hipError_t launch_attention(DType dt, const AttnArgs& a, hipStream_t s);
+
+// GroupNorm statistics over up to two channel-concatenated NHWC sources;
+// writes per-(img, channel) scale = gamma*rstd and shift = beta - mean*scale.
+hipError_t launch_groupnorm_stats(DType dt, const void* src0, int c0, const void* src1, int c1,
+                                  int imgs, int hw, int groups, float eps, const float* gamma,
+                                  const float* beta, float* partial, float* scale, float* shift,
+                                  hipStream_t s);
+size_t groupnorm_partial_floats(int imgs, int hw, int cin);
+
+hipError_t launch_layernorm(DType dt, const void* x, void* y, long tokens, int C, const float* gamma,
+                            const float* beta, float eps, hipStream_t s);
+
+// y[t, j] = x[t, j] * gelu(x[t, half + j]), j < half; x is [tokens, 2*half].
+hipError_t launch_geglu(DType dt, const void* x, void* y, long tokens, int half, hipStream_t s);
+
+// Per-row scalars of a step (device arrays in the workspace).
+struct RowMaps {
+  const int* row_req;     // [rows]
+  const int* row_branch;  // [rows]
+  const int* row_ctx;     // [rows]
+  const float* row_t;     // [rows]
+  const int* req_row_u;   // [n_req]
+  const float* req_coef;  // [n_req, 3] = (A, B, w)
+};
+
+hipError_t launch_pack_latents(DType dt, const float* lat, void* x0, int rows, int lc, int hw,
+                               int cpad, const int* row_req, hipStream_t s);
+// e[row, :] = [cos(t f_i) | sin(t f_i)] (+ [pooled | sinusoids of time ids] for add_in)
+hipError_t launch_time_inputs(const float* row_t, int rows, int temb_in, float* e,
+                              const float* pooled_cond, const float* pooled_uncond,
+                              const int* row_req, const int* row_branch, int pooled_dim,
+                              const float* time_ids_dev, int n_ids, int id_dim, float* a,
+                              hipStream_t s);
+// out[m, n] = act_out(sum_k act_in(in[m, k]) W[n, k] + bias[n] + add[m, n]); M <= 128.
+hipError_t launch_linear_smallm(DType wdt, const float* in, int M, int K, const void* W,
+                                const float* bias, const float* add, float* out, int N,
+                                int silu_in, int silu_out, hipStream_t s);
+hipError_t launch_cfg_ddim(const float* eps_rows, const float* lat_in, float* lat_out,
+                           float* eps_out, int n_req, int lc, int hw, const int* req_row_u,
+                           const float* req_coef, hipStream_t s);
+
+}  // namespace sd

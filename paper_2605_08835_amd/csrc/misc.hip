@@ -1,0 +1,386 @@
+// Memory-bound kernels of the step: row packing, time-embedding inputs and
+// small-M MLP, GroupNorm statistics, LayerNorm, GEGLU and the fused CFG
+// combine + DDIM update.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace sd {
+
+// ------------------------------------------------------------ row packing
+// x0[row, p, c] = latents[row_req[row], c, p] for c < lc, 0 for lc <= c < cpad.
+template <typename T>
+__global__ void pack_latents_kernel(const float* lat, T* x0, int rows, int lc, int hw, int cpad,
+                                    const int* row_req) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (long)rows * hw) return;
+  const int row = (int)(i / hw), p = (int)(i - (long)row * hw);
+  const int r = row_req[row];
+  for (int c = 0; c < cpad; ++c) {
+    const float v = c < lc ? lat[((long)r * lc + c) * hw + p] : 0.f;
+    x0[i * cpad + c] = from_f<T>(v);
+  }
+}
+
+hipError_t launch_pack_latents(DType dt, const float* lat, void* x0, int rows, int lc, int hw,
+                               int cpad, const int* row_req, hipStream_t s) {
+  const long n = (long)rows * hw;
+  if (n == 0) return hipSuccess;
+  const unsigned blocks = (unsigned)((n + 255) / 256);
+  if (dt == BF16)
+    pack_latents_kernel<bf16><<<blocks, 256, 0, s>>>(lat, (bf16*)x0, rows, lc, hw, cpad, row_req);
+  else
+    pack_latents_kernel<float><<<blocks, 256, 0, s>>>(lat, (float*)x0, rows, lc, hw, cpad, row_req);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------ time-embedding inputs
+// Sinusoid [cos(t f_i) | sin(t f_i)], f_i = 10000^(-i/half), evaluated in
+// fp64 so the argument t f_i (up to ~1e3 rad) keeps full fp32 accuracy.
+__device__ inline void sinusoid(double t, int dim, float* out) {
+  const int half = dim / 2;
+  for (int i = 0; i < half; ++i) {
+    const double f = exp(-9.210340371976184 * (double)i / (double)half);  // ln(1e4)
+    double sv, cv;
+    sincos(t * f, &sv, &cv);
+    out[i] = (float)cv;
+    out[half + i] = (float)sv;
+  }
+}
+
+__global__ void time_inputs_kernel(const float* row_t, int rows, int temb_in, float* e,
+                                   const float* pooled_cond, const float* pooled_uncond,
+                                   const int* row_req, const int* row_branch, int pooled_dim,
+                                   const float* time_ids, int n_ids, int id_dim, float* a) {
+  const int row = blockIdx.x;
+  if (row >= rows) return;
+  if (threadIdx.x == 0) sinusoid((double)row_t[row], temb_in, e + (long)row * temb_in);
+  if (a) {
+    const int add_in = pooled_dim + n_ids * id_dim;
+    float* ar = a + (long)row * add_in;
+    const float* pooled = row_branch[row] ? pooled_uncond : pooled_cond + (long)row_req[row] * pooled_dim;
+    for (int i = threadIdx.x; i < pooled_dim; i += blockDim.x) ar[i] = pooled[i];
+    if (threadIdx.x < n_ids)
+      sinusoid((double)time_ids[threadIdx.x], id_dim, ar + pooled_dim + threadIdx.x * id_dim);
+  }
+}
+
+hipError_t launch_time_inputs(const float* row_t, int rows, int temb_in, float* e,
+                              const float* pooled_cond, const float* pooled_uncond,
+                              const int* row_req, const int* row_branch, int pooled_dim,
+                              const float* time_ids_dev, int n_ids, int id_dim, float* a,
+                              hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  time_inputs_kernel<<<rows, 64, 0, s>>>(row_t, rows, temb_in, e, pooled_cond, pooled_uncond,
+                                         row_req, row_branch, pooled_dim, time_ids_dev, n_ids,
+                                         id_dim, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------- small-M linear
+// out[m, n] = act_out(sum_k act_in(in[m, k]) W[n, k] + bias[n] + add[m, n]).
+// 64 columns per block; each thread owns one column and rows rg + 4 i.
+// Weights stream once; the input is staged in LDS 64 K-columns at a time.
+namespace sm {
+constexpr int MMAX = 128, KC = 64;
+}
+
+template <typename TW>
+__global__ __launch_bounds__(256) void linear_smallm_kernel(const float* in, int M, int K, const TW* W,
+                                                            const float* bias, const float* add,
+                                                            float* out, int N, int silu_in,
+                                                            int silu_out) {
+  using namespace sm;
+  __shared__ float xs[MMAX][KC + 1];
+  const int tid = threadIdx.x, cn = tid & 63, rg = tid >> 6;
+  const int n = blockIdx.x * 64 + cn;
+  float acc[MMAX / 4];
+#pragma unroll
+  for (int i = 0; i < MMAX / 4; ++i) acc[i] = 0.f;
+  for (int k0 = 0; k0 < K; k0 += KC) {
+    __syncthreads();
+    for (int idx = tid; idx < M * KC; idx += 256) {
+      const int m = idx / KC, kk = idx - m * KC;
+      float v = (k0 + kk < K) ? in[(long)m * K + k0 + kk] : 0.f;
+      if (silu_in) v = silu_f(v);
+      xs[m][kk] = v;
+    }
+    __syncthreads();
+    if (n < N) {
+      for (int kk = 0; kk < KC; kk += 8) {
+        float w[8];
+        if (k0 + kk < K) {
+          load8f(W + (long)n * K + k0 + kk, w);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) w[i] = 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < MMAX / 4; ++i) {
+          const int m = rg + 4 * i;
+          if (m < M) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc[i] = fmaf(xs[m][kk + j], w[j], acc[i]);
+          }
+        }
+      }
+    }
+  }
+  if (n >= N) return;
+#pragma unroll
+  for (int i = 0; i < MMAX / 4; ++i) {
+    const int m = rg + 4 * i;
+    if (m < M) {
+      float v = acc[i] + (bias ? bias[n] : 0.f) + (add ? add[(long)m * N + n] : 0.f);
+      if (silu_out) v = silu_f(v);
+      out[(long)m * N + n] = v;
+    }
+  }
+}
+
+hipError_t launch_linear_smallm(DType wdt, const float* in, int M, int K, const void* W,
+                                const float* bias, const float* add, float* out, int N,
+                                int silu_in, int silu_out, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (M > sm::MMAX || K % 8) return hipErrorInvalidValue;
+  const unsigned blocks = (unsigned)((N + 63) / 64);
+  if (wdt == BF16)
+    linear_smallm_kernel<bf16><<<blocks, 256, 0, s>>>(in, M, K, (const bf16*)W, bias, add, out, N,
+                                                      silu_in, silu_out);
+  else
+    linear_smallm_kernel<float><<<blocks, 256, 0, s>>>(in, M, K, (const float*)W, bias, add, out,
+                                                       N, silu_in, silu_out);
+  return hipGetLastError();
+}
+
+// --------------------------------------------------------- GroupNorm stats
+// Pass 1: per (img, pixel chunk) fp32 sums and sums of squares per channel.
+// Threads (cv, pp): channel vector cv (8 channels, one 16-byte load) of
+// pixels p0 + pp, p0 + pp + PP, ...; partial results reduced over pp in LDS.
+static inline int gn_splits(int hw) {
+  int s = (hw + 63) / 64;
+  return s < 1 ? 1 : (s > 64 ? 64 : s);
+}
+
+size_t groupnorm_partial_floats(int imgs, int hw, int cin) {
+  return (size_t)imgs * gn_splits(hw) * cin * 2;
+}
+
+template <typename T>
+__global__ void gn_partial_kernel(const T* src0, int c0, const T* src1, int c1, int hw, int nsplit,
+                                  int PP, float* partial) {
+  extern __shared__ float red[];  // [PP][cin][2]
+  const int cin = c0 + c1, CV = cin / 8;
+  const int img = blockIdx.y, split = blockIdx.x;
+  const int chunk = (hw + nsplit - 1) / nsplit;
+  const int p0 = split * chunk, p1 = min(hw, p0 + chunk);
+  const int cv = threadIdx.x % CV, pp = threadIdx.x / CV;
+  const int c = cv * 8;
+  float s[8] = {}, q[8] = {};
+  if (pp < PP) {
+    for (int p = p0 + pp; p < p1; p += PP) {
+      float v[8];
+      const long pix = (long)img * hw + p;
+      if (c < c0)
+        load8f(src0 + pix * c0 + c, v);
+      else
+        load8f(src1 + pix * c1 + (c - c0), v);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        s[i] += v[i];
+        q[i] = fmaf(v[i], v[i], q[i]);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      red[((long)pp * cin + c + i) * 2] = s[i];
+      red[((long)pp * cin + c + i) * 2 + 1] = q[i];
+    }
+  }
+  __syncthreads();
+  for (int ch = threadIdx.x; ch < cin; ch += blockDim.x) {
+    float ss = 0.f, qq = 0.f;
+    for (int k = 0; k < PP; ++k) {
+      ss += red[((long)k * cin + ch) * 2];
+      qq += red[((long)k * cin + ch) * 2 + 1];
+    }
+    float* o = partial + (((long)img * nsplit + split) * cin + ch) * 2;
+    o[0] = ss;
+    o[1] = qq;
+  }
+}
+
+// Pass 2: one wave per group merges the partials in fp64 and writes the
+// per-(img, channel) affine scale = gamma * rstd, shift = beta - mean * scale.
+__global__ void gn_finalize_kernel(const float* partial, int cin, int nsplit, int hw, int groups,
+                                   float eps, const float* gamma, const float* beta, float* scale,
+                                   float* shift) {
+  const int img = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int cpg = cin / groups;
+  for (int g = wave; g < groups; g += blockDim.x / 64) {
+    double s = 0.0, q = 0.0;
+    for (int idx = lane; idx < nsplit * cpg; idx += 64) {
+      const int sp = idx / cpg, ch = g * cpg + (idx - sp * cpg);
+      const float* p = partial + (((long)img * nsplit + sp) * cin + ch) * 2;
+      s += p[0];
+      q += p[1];
+    }
+    s = wave_sum_d(s);
+    q = wave_sum_d(q);
+    const double n = (double)cpg * hw;
+    const double mean = s / n;
+    double var = q / n - mean * mean;
+    if (var < 0.0) var = 0.0;
+    const float rstd = (float)(1.0 / sqrt(var + (double)eps));
+    for (int ch = g * cpg + lane; ch < (g + 1) * cpg; ch += 64) {
+      const float sc = gamma[ch] * rstd;
+      scale[(long)img * cin + ch] = sc;
+      shift[(long)img * cin + ch] = beta[ch] - (float)mean * sc;
+    }
+  }
+}
+
+hipError_t launch_groupnorm_stats(DType dt, const void* src0, int c0, const void* src1, int c1,
+                                  int imgs, int hw, int groups, float eps, const float* gamma,
+                                  const float* beta, float* partial, float* scale, float* shift,
+                                  hipStream_t s) {
+  if (imgs == 0) return hipSuccess;
+  const int cin = c0 + c1, CV = cin / 8;
+  const int PP = CV >= 256 ? 1 : 256 / CV;
+  const int nsplit = gn_splits(hw);
+  const int threads = CV * PP;
+  const size_t lds = (size_t)PP * cin * 2 * sizeof(float);
+  if (threads > 1024 || lds > 64 * 1024) return hipErrorInvalidValue;
+  dim3 grid(nsplit, imgs);
+  if (dt == BF16)
+    gn_partial_kernel<bf16><<<grid, threads, lds, s>>>((const bf16*)src0, c0, (const bf16*)src1, c1,
+                                                       hw, nsplit, PP, partial);
+  else
+    gn_partial_kernel<float><<<grid, threads, lds, s>>>((const float*)src0, c0, (const float*)src1,
+                                                        c1, hw, nsplit, PP, partial);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  gn_finalize_kernel<<<imgs, 256, 0, s>>>(partial, cin, nsplit, hw, groups, eps, gamma, beta, scale,
+                                          shift);
+  return hipGetLastError();
+}
+
+// -------------------------------------------------------------- LayerNorm
+// One wave per token; the token's C values stay in registers (C <= 2048).
+template <typename T>
+__global__ __launch_bounds__(256) void layernorm_kernel(const T* x, T* y, long tokens, int C,
+                                                        const float* gamma, const float* beta,
+                                                        float eps) {
+  constexpr int MAXV = 4;
+  const long t = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= tokens) return;
+  const int CV = C / 8;
+  float v[MAXV][8];
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < MAXV; ++j) {
+    const int cv = lane + 64 * j;
+    if (cv < CV) {
+      load8f(x + t * C + cv * 8, v[j]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s += v[j][i];
+    }
+  }
+  const float mean = wave_sum(s) / C;
+  float q = 0.f;
+#pragma unroll
+  for (int j = 0; j < MAXV; ++j)
+    if (lane + 64 * j < CV)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float d = v[j][i] - mean;
+        q = fmaf(d, d, q);
+      }
+  const float rstd = rsqrtf(wave_sum(q) / C + eps);
+#pragma unroll
+  for (int j = 0; j < MAXV; ++j) {
+    const int cv = lane + 64 * j;
+    if (cv < CV) {
+      float g[8], b[8], o[8];
+      load8f(gamma + cv * 8, g);
+      load8f(beta + cv * 8, b);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[i] = (v[j][i] - mean) * rstd * g[i] + b[i];
+      store8f(y + t * C + cv * 8, o);
+    }
+  }
+}
+
+hipError_t launch_layernorm(DType dt, const void* x, void* y, long tokens, int C, const float* gamma,
+                            const float* beta, float eps, hipStream_t s) {
+  if (tokens == 0) return hipSuccess;
+  if (C % 8 || C > 2048) return hipErrorInvalidValue;
+  const unsigned blocks = (unsigned)((tokens + 3) / 4);
+  if (dt == BF16)
+    layernorm_kernel<bf16><<<blocks, 256, 0, s>>>((const bf16*)x, (bf16*)y, tokens, C, gamma, beta, eps);
+  else
+    layernorm_kernel<float><<<blocks, 256, 0, s>>>((const float*)x, (float*)y, tokens, C, gamma, beta,
+                                                   eps);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ GEGLU
+template <typename T>
+__global__ void geglu_kernel(const T* x, T* y, long tokens, int half) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;  // one 8-vector
+  const int hv = half / 8;
+  if (i >= tokens * hv) return;
+  const long t = i / hv;
+  const int j = (int)(i - t * hv) * 8;
+  float a[8], g[8], o[8];
+  load8f(x + t * 2 * half + j, a);
+  load8f(x + t * 2 * half + half + j, g);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) o[k] = a[k] * (0.5f * g[k] * (1.0f + erff(g[k] * 0.70710678118654752f)));
+  store8f(y + t * half + j, o);
+}
+
+hipError_t launch_geglu(DType dt, const void* x, void* y, long tokens, int half, hipStream_t s) {
+  const long n = tokens * (half / 8);
+  if (n == 0) return hipSuccess;
+  const unsigned blocks = (unsigned)((n + 255) / 256);
+  if (dt == BF16)
+    geglu_kernel<bf16><<<blocks, 256, 0, s>>>((const bf16*)x, (bf16*)y, tokens, half);
+  else
+    geglu_kernel<float><<<blocks, 256, 0, s>>>((const float*)x, (float*)y, tokens, half);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------ CFG combine + DDIM
+// eps = cfg ? eps_u + w (eps_c - eps_u) : eps_c;  x' = A x + B eps.
+__global__ void cfg_ddim_kernel(const float* eps_rows, const float* lat_in, float* lat_out,
+                                float* eps_out, int n_req, int lc, int hw, const int* req_row_u,
+                                const float* req_coef) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (long)n_req * hw) return;
+  const int r = (int)(i / hw), p = (int)(i - (long)r * hw);
+  const int ru = req_row_u[r];
+  const float A = req_coef[3 * r], B = req_coef[3 * r + 1], w = req_coef[3 * r + 2];
+  const float* ec = eps_rows + ((long)r * hw + p) * lc;
+  const float* eu = ru >= 0 ? eps_rows + ((long)ru * hw + p) * lc : nullptr;
+  for (int c = 0; c < lc; ++c) {
+    float e = ec[c];
+    if (eu) e = eu[c] + w * (e - eu[c]);
+    const long o = ((long)r * lc + c) * hw + p;
+    const float x = lat_in[o];
+    lat_out[o] = A * x + B * e;
+    if (eps_out) eps_out[o] = e;
+  }
+}
+
+hipError_t launch_cfg_ddim(const float* eps_rows, const float* lat_in, float* lat_out,
+                           float* eps_out, int n_req, int lc, int hw, const int* req_row_u,
+                           const float* req_coef, hipStream_t s) {
+  const long n = (long)n_req * hw;
+  if (n == 0) return hipSuccess;
+  cfg_ddim_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(eps_rows, lat_in, lat_out, eps_out, n_req,
+                                                              lc, hw, req_row_u, req_coef);
+  return hipGetLastError();
+}
+
+}  // namespace sd

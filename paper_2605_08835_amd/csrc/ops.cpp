@@ -1,0 +1,113 @@
+// Kernel-level C entry points (synerdiff_ops.h): validation + one launch.
+#include <hip/hip_runtime_api.h>
+#include <string.h>
+
+#include <string>
+
+#include "kernels.h"
+#include "synerdiff_ops.h"
+
+namespace sd {
+extern thread_local std::string g_err;
+}
+using namespace sd;
+
+static sd_status op_fail(sd_status s, const char* m) {
+  g_err = m;
+  return s;
+}
+static sd_status op_hip(hipError_t e, const char* w) {
+  if (e == hipSuccess) return SD_OK;
+  g_err = std::string(w) + ": " + hipGetErrorString(e);
+  return SD_ERR_HIP;
+}
+static bool bad_dtype(int32_t d) { return d != SD_F32 && d != SD_BF16; }
+
+extern "C" {
+
+sd_status synerdiff_op_conv(int32_t dtype, const void* x0, int32_t c0, const void* x1, int32_t c1, int32_t n,
+                            int32_t H, int32_t W, int32_t ks, int32_t stride, int32_t up, const float* scale,
+                            const float* shift, int32_t silu, const void* w, int32_t cout, const float* bias,
+                            const void* resid, void* out, int32_t out_f32, void* stream) {
+  if (bad_dtype(dtype)) return op_fail(SD_ERR_INVALID_ARG, "bad dtype");
+  if (!x0 || !w || !out || (c1 && !x1) || (!scale) != (!shift)) return op_fail(SD_ERR_INVALID_ARG, "NULL argument");
+  if (n < 0 || H < 1 || W < 1 || c0 < 8 || c0 % 8 || c1 < 0 || c1 % 8 || cout < 1)
+    return op_fail(SD_ERR_INVALID_ARG, "bad shape");
+  if ((ks != 1 && ks != 3) || (stride != 1 && stride != 2) || (up && stride != 1) || (ks == 1 && (stride != 1 || up)))
+    return op_fail(SD_ERR_UNSUPPORTED, "unsupported ks/stride/up");
+  if (stride == 2 && (H % 2 || W % 2)) return op_fail(SD_ERR_UNSUPPORTED, "stride 2 needs even H, W");
+  if (n == 0) return SD_OK;
+  GemmArgs a;
+  memset(&a, 0, sizeof(a));
+  ASeg& s = a.seg[0];
+  s.src0 = x0; s.src1 = x1; s.c0 = c0; s.c1 = c1; s.cin = c0 + c1;
+  s.scale = scale; s.shift = shift; s.silu = silu ? 1 : 0;
+  s.ks = ks; s.stride = stride; s.up = up ? 1 : 0;
+  s.Hi = H; s.Wi = W;
+  s.Ho = up ? 2 * H : H / stride;
+  s.Wo = up ? 2 * W : W / stride;
+  s.K = ks * ks * s.cin;
+  const long M = (long)n * s.Ho * s.Wo;
+  if (M > 0x7FFFFFFFL) return op_fail(SD_ERR_UNSUPPORTED, "too many output pixels");
+  a.M = (int)M; a.N = cout; a.K = s.K; a.B = w; a.ldb = s.K;
+  a.epi.bias = bias; a.epi.resid = resid; a.epi.ldr = cout; a.epi.out = out; a.epi.ldo = cout;
+  a.epi.out_f32 = out_f32 ? 1 : 0; a.epi.hw = 1;
+  return op_hip(launch_gemm((DType)dtype, a, (hipStream_t)stream), "conv");
+}
+
+sd_status synerdiff_op_attention(int32_t dtype, const void* q, int64_t q_ld, int64_t q_img, const void* k,
+                                 const void* v, int64_t kv_ld, int64_t kv_img, const int32_t* kv_index, void* o,
+                                 int64_t o_ld, int64_t o_img, int32_t n, int32_t heads, int32_t d, int32_t nq,
+                                 int32_t nk, float scale, void* stream) {
+  if (bad_dtype(dtype)) return op_fail(SD_ERR_INVALID_ARG, "bad dtype");
+  if (!q || !k || !v || !o) return op_fail(SD_ERR_INVALID_ARG, "NULL argument");
+  if (n < 0 || heads < 1 || d < 8 || d % 8 || nq < 0 || nk < 1) return op_fail(SD_ERR_INVALID_ARG, "bad shape");
+  const int dp = (d + 31) / 32 * 32;
+  if (dtype == SD_BF16 ? (dp > 256 || dp == 224) : d > 64) return op_fail(SD_ERR_UNSUPPORTED, "unsupported head width");
+  if (n == 0 || nq == 0) return SD_OK;
+  AttnArgs a;
+  a.q = q; a.q_ld = q_ld; a.q_img = q_img;
+  a.k = k; a.v = v; a.kv_ld = kv_ld; a.kv_img = kv_img; a.kv_index = kv_index;
+  a.o = o; a.o_ld = o_ld; a.o_img = o_img;
+  a.imgs = n; a.heads = heads; a.d = d; a.Nq = nq; a.Nk = nk; a.scale = scale;
+  return op_hip(launch_attention((DType)dtype, a, (hipStream_t)stream), "attention");
+}
+
+size_t synerdiff_op_groupnorm_scratch_floats(int32_t n, int32_t hw, int32_t cin) {
+  if (n < 0 || hw < 1 || cin < 1) return 0;
+  return groupnorm_partial_floats(n, hw, cin);
+}
+
+sd_status synerdiff_op_groupnorm_stats(int32_t dtype, const void* x0, int32_t c0, const void* x1, int32_t c1,
+                                       int32_t n, int32_t hw, int32_t groups, float eps, const float* gamma,
+                                       const float* beta, float* partial, float* scale, float* shift,
+                                       void* stream) {
+  if (bad_dtype(dtype)) return op_fail(SD_ERR_INVALID_ARG, "bad dtype");
+  if (!x0 || (c1 && !x1) || !gamma || !beta || !partial || !scale || !shift)
+    return op_fail(SD_ERR_INVALID_ARG, "NULL argument");
+  const int cin = c0 + c1;
+  if (n < 0 || hw < 1 || c0 < 8 || c0 % 8 || c1 < 0 || c1 % 8 || groups < 1 || cin % groups)
+    return op_fail(SD_ERR_INVALID_ARG, "bad shape");
+  if (cin > 4096) return op_fail(SD_ERR_UNSUPPORTED, "too many channels");
+  if (n == 0) return SD_OK;
+  return op_hip(launch_groupnorm_stats((DType)dtype, x0, c0, x1, c1, n, hw, groups, eps, gamma, beta, partial,
+                                       scale, shift, (hipStream_t)stream),
+                "groupnorm");
+}
+
+sd_status synerdiff_op_layernorm(int32_t dtype, const void* x, void* y, int64_t tokens, int32_t C,
+                                 const float* gamma, const float* beta, float eps, void* stream) {
+  if (bad_dtype(dtype)) return op_fail(SD_ERR_INVALID_ARG, "bad dtype");
+  if (!x || !y || !gamma || !beta) return op_fail(SD_ERR_INVALID_ARG, "NULL argument");
+  if (tokens < 0 || C < 8 || C % 8 || C > 2048) return op_fail(SD_ERR_INVALID_ARG, "bad shape");
+  return op_hip(launch_layernorm((DType)dtype, x, y, tokens, C, gamma, beta, eps, (hipStream_t)stream), "layernorm");
+}
+
+sd_status synerdiff_op_geglu(int32_t dtype, const void* x, void* y, int64_t tokens, int32_t half, void* stream) {
+  if (bad_dtype(dtype)) return op_fail(SD_ERR_INVALID_ARG, "bad dtype");
+  if (!x || !y) return op_fail(SD_ERR_INVALID_ARG, "NULL argument");
+  if (tokens < 0 || half < 8 || half % 8) return op_fail(SD_ERR_INVALID_ARG, "bad shape");
+  return op_hip(launch_geglu((DType)dtype, x, y, tokens, half, (hipStream_t)stream), "geglu");
+}
+
+}  // extern "C"

@@ -1,0 +1,1019 @@
+// Host runtime of the UNet step: weight packing, workspace planning, the
+// per-step row plan and the launch sequence.  All device work is enqueued on
+// the caller's stream; the only host<->device traffic per step is one small
+// H2D copy of the per-row scalars from a pinned staging ring.
+#include <hip/hip_runtime_api.h>
+#include <math.h>
+#include <string.h>
+
+#include <cmath>
+
+#include <algorithm>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "manifest.h"
+#include "synerdiff.h"
+
+namespace sd {
+
+thread_local std::string g_err;
+
+static sd_status fail(sd_status s, const std::string& m) {
+  g_err = m;
+  return s;
+}
+
+static inline uint16_t f2bf(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  if ((u & 0x7F800000u) == 0x7F800000u) return (uint16_t)((u >> 16) | ((u & 0xFFFF) ? 0x40 : 0));
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// ------------------------------------------------------------------ layout
+enum PackKind { P_ACT, P_F32, P_F32_SUM, P_CONV3, P_CONV3_SKIP };
+struct PackJob {
+  PackKind kind;
+  size_t dst;
+  std::vector<std::string> names;
+  int cin_pad;
+};
+
+struct ConvW {
+  size_t w = 0, b = 0;
+  int cin = 0, cout = 0, K = 0;
+};
+struct ResW {
+  int cin = 0, cout = 0;
+  size_t n1g = 0, n1b = 0, n2g = 0, n2b = 0;
+  ConvW c1, c2;  // c2 holds [conv2 | skip] along K when the width changes
+  bool skip = false;
+  int tb_off = 0;
+};
+struct BlkW {
+  size_t ln1g, ln1b, qkv, o1w, o1b, ln2g, ln2b, q2, kv2, o2w, o2b, ln3g, ln3b, f1w, f1b, f2w, f2b;
+};
+struct TxW {
+  int C = 0, heads = 0, d = 0;
+  size_t ng = 0, nb = 0, piw = 0, pib = 0, pow = 0, pob = 0;
+  std::vector<BlkW> blk;
+};
+struct LevelW {
+  std::vector<ResW> res;
+  std::vector<TxW> tx;  // empty when the level has no transformer
+  bool has_conv = false;
+  ConvW conv;  // downsample (down path) or upsample conv (up path)
+};
+
+// Workspace roles (buffers sized by a dry run at max capacity).
+enum Role {
+  R_X0, R_HA, R_HB, R_U, R_TZ, R_TX, R_TQ, R_TF, R_CTX, R_CKV, R_GNP, R_GNS, R_GNH,
+  R_E, R_A, R_H1, R_TAU, R_T2, R_TB, R_EPS, R_SCAL, R_SKIP0
+};
+
+}  // namespace sd
+
+struct sd_unet {
+  sd_unet_config cfg;
+  sd::DType dt;
+  int esz;  // activation element size
+  uint8_t* wdev;
+  size_t wbytes;
+  uint8_t* ws;
+  size_t wsbytes;
+  std::vector<sd::Param> manifest;
+  std::vector<sd::PackJob> jobs;
+  size_t wtotal = 0;
+  // network
+  sd::ConvW conv_in;
+  std::vector<sd::LevelW> down, up;
+  sd::ResW mid0, mid1;
+  std::vector<sd::TxW> midtx;
+  size_t outg = 0, outb = 0;
+  sd::ConvW conv_out;
+  size_t t1w, t1b, t2w, t2b, a1w = 0, a1b = 0, a2w = 0, a2b = 0, tbw, tbb;
+  int tb_total = 0;
+  int cpad = 8;
+  int n_skips = 0;
+  // workspace
+  std::map<int, size_t> need, off;
+  size_t scal_bytes = 0;
+  // profiling: one event after every launch; consecutive events bound it
+  struct Rec {
+    int kind;  // -1: start-of-step marker
+    double flops, bytes;
+    hipEvent_t ev;
+  };
+  bool prof = false;
+  std::vector<hipEvent_t> pool;
+  std::vector<Rec> recs;
+  struct Tot {
+    long launches = 0;
+    double ms = 0, flops = 0, bytes = 0;
+  } tot[16];
+  // staging
+  static constexpr int SLOTS = 8;
+  uint8_t* pinned = nullptr;
+  hipEvent_t ev[SLOTS] = {};
+  int slot = 0;
+};
+
+namespace sd {
+
+// ----------------------------------------------------------- weight arena
+static size_t walloc(sd_unet* h, size_t bytes) {
+  const size_t o = align256(h->wtotal);
+  h->wtotal = o + bytes;
+  return o;
+}
+static size_t job_act(sd_unet* h, std::vector<std::string> names, size_t numel) {
+  const size_t d = walloc(h, numel * h->esz);
+  h->jobs.push_back(PackJob{P_ACT, d, std::move(names), 0});
+  return d;
+}
+static size_t job_f32(sd_unet* h, std::vector<std::string> names, size_t numel, bool sum = false) {
+  const size_t d = walloc(h, numel * 4);
+  h->jobs.push_back(PackJob{sum ? P_F32_SUM : P_F32, d, std::move(names), 0});
+  return d;
+}
+
+static ConvW conv3(sd_unet* h, const std::string& p, int cin, int cout, int cin_pad) {
+  ConvW c;
+  c.cin = cin_pad;
+  c.cout = cout;
+  c.K = 9 * cin_pad;
+  c.w = walloc(h, (size_t)cout * c.K * h->esz);
+  h->jobs.push_back(PackJob{P_CONV3, c.w, {p + ".w"}, cin_pad});
+  c.b = job_f32(h, {p + ".b"}, cout);
+  return c;
+}
+
+static ResW resblock(sd_unet* h, const std::string& p, int cin, int cout, int& tb_off,
+                     std::vector<std::string>& temb_names) {
+  ResW r;
+  r.cin = cin;
+  r.cout = cout;
+  r.skip = cin != cout;
+  r.n1g = job_f32(h, {p + ".norm1.g"}, cin);
+  r.n1b = job_f32(h, {p + ".norm1.b"}, cin);
+  r.c1 = conv3(h, p + ".conv1", cin, cout, cin);
+  r.n2g = job_f32(h, {p + ".norm2.g"}, cout);
+  r.n2b = job_f32(h, {p + ".norm2.b"}, cout);
+  r.c2.cin = cout;
+  r.c2.cout = cout;
+  r.c2.K = 9 * cout + (r.skip ? cin : 0);
+  r.c2.w = walloc(h, (size_t)cout * r.c2.K * h->esz);
+  if (r.skip) {
+    h->jobs.push_back(PackJob{P_CONV3_SKIP, r.c2.w, {p + ".conv2.w", p + ".skip.w"}, cout});
+    r.c2.b = job_f32(h, {p + ".conv2.b", p + ".skip.b"}, cout, true);
+  } else {
+    h->jobs.push_back(PackJob{P_CONV3, r.c2.w, {p + ".conv2.w"}, cout});
+    r.c2.b = job_f32(h, {p + ".conv2.b"}, cout);
+  }
+  r.tb_off = tb_off;
+  tb_off += cout;
+  temb_names.push_back(p + ".temb");
+  return r;
+}
+
+static TxW transformer(sd_unet* h, const std::string& p, int C, int depth) {
+  const sd_unet_config& c = h->cfg;
+  TxW t;
+  t.C = C;
+  t.heads = heads_at(c, C);
+  t.d = C / t.heads;
+  const size_t CC = (size_t)C * C;
+  t.ng = job_f32(h, {p + ".norm.g"}, C);
+  t.nb = job_f32(h, {p + ".norm.b"}, C);
+  t.piw = job_act(h, {p + ".proj_in.w"}, CC);
+  t.pib = job_f32(h, {p + ".proj_in.b"}, C);
+  for (int j = 0; j < depth; ++j) {
+    const std::string b = p + ".blk" + std::to_string(j);
+    BlkW w;
+    w.ln1g = job_f32(h, {b + ".ln1.g"}, C);
+    w.ln1b = job_f32(h, {b + ".ln1.b"}, C);
+    w.qkv = job_act(h, {b + ".attn1.q.w", b + ".attn1.k.w", b + ".attn1.v.w"}, 3 * CC);
+    w.o1w = job_act(h, {b + ".attn1.o.w"}, CC);
+    w.o1b = job_f32(h, {b + ".attn1.o.b"}, C);
+    w.ln2g = job_f32(h, {b + ".ln2.g"}, C);
+    w.ln2b = job_f32(h, {b + ".ln2.b"}, C);
+    w.q2 = job_act(h, {b + ".attn2.q.w"}, CC);
+    w.kv2 = job_act(h, {b + ".attn2.k.w", b + ".attn2.v.w"}, (size_t)2 * C * c.ctx_dim);
+    w.o2w = job_act(h, {b + ".attn2.o.w"}, CC);
+    w.o2b = job_f32(h, {b + ".attn2.o.b"}, C);
+    w.ln3g = job_f32(h, {b + ".ln3.g"}, C);
+    w.ln3b = job_f32(h, {b + ".ln3.b"}, C);
+    w.f1w = job_act(h, {b + ".ff.w1"}, 8 * CC);
+    w.f1b = job_f32(h, {b + ".ff.b1"}, 8 * C);
+    w.f2w = job_act(h, {b + ".ff.w2"}, 4 * CC);
+    w.f2b = job_f32(h, {b + ".ff.b2"}, C);
+    t.blk.push_back(w);
+  }
+  t.pow = job_act(h, {p + ".proj_out.w"}, CC);
+  t.pob = job_f32(h, {p + ".proj_out.b"}, C);
+  return t;
+}
+
+static void build_layout(sd_unet* h) {
+  const sd_unet_config& c = h->cfg;
+  const int td = c.temb_dim, nl = c.n_levels;
+  h->t1w = job_act(h, {"time.lin1.w"}, (size_t)td * c.temb_in);
+  h->t1b = job_f32(h, {"time.lin1.b"}, td);
+  h->t2w = job_act(h, {"time.lin2.w"}, (size_t)td * td);
+  h->t2b = job_f32(h, {"time.lin2.b"}, td);
+  if (c.add_in) {
+    h->a1w = job_act(h, {"add.lin1.w"}, (size_t)td * c.add_in);
+    h->a1b = job_f32(h, {"add.lin1.b"}, td);
+    h->a2w = job_act(h, {"add.lin2.w"}, (size_t)td * td);
+    h->a2b = job_f32(h, {"add.lin2.b"}, td);
+  }
+  h->conv_in = conv3(h, "conv_in", c.latent_c, c.ch[0], h->cpad);
+  int tb = 0;
+  std::vector<std::string> temb;
+  std::vector<int> skips{c.ch[0]};
+  int cur = c.ch[0];
+  h->down.resize(nl);
+  for (int l = 0; l < nl; ++l) {
+    const std::string p = "down" + std::to_string(l);
+    for (int i = 0; i < c.n_res; ++i) {
+      h->down[l].res.push_back(resblock(h, p + ".res" + std::to_string(i), cur, c.ch[l], tb, temb));
+      cur = c.ch[l];
+      if (c.tx_depth[l]) h->down[l].tx.push_back(transformer(h, p + ".tx" + std::to_string(i), cur, c.tx_depth[l]));
+      skips.push_back(cur);
+    }
+    if (l != nl - 1) {
+      h->down[l].has_conv = true;
+      h->down[l].conv = conv3(h, p + ".down", cur, cur, cur);
+      skips.push_back(cur);
+    }
+  }
+  h->n_skips = (int)skips.size();
+  h->mid0 = resblock(h, "mid.res0", cur, cur, tb, temb);
+  if (c.mid_tx_depth) h->midtx.push_back(transformer(h, "mid.tx", cur, c.mid_tx_depth));
+  h->mid1 = resblock(h, "mid.res1", cur, cur, tb, temb);
+  h->up.resize(nl);
+  for (int l = nl - 1; l >= 0; --l) {
+    const std::string p = "up" + std::to_string(l);
+    for (int i = 0; i <= c.n_res; ++i) {
+      const int s = skips.back();
+      skips.pop_back();
+      h->up[l].res.push_back(resblock(h, p + ".res" + std::to_string(i), cur + s, c.ch[l], tb, temb));
+      cur = c.ch[l];
+      if (c.tx_depth[l]) h->up[l].tx.push_back(transformer(h, p + ".tx" + std::to_string(i), cur, c.tx_depth[l]));
+    }
+    if (l != 0) {
+      h->up[l].has_conv = true;
+      h->up[l].conv = conv3(h, p + ".up", cur, cur, cur);
+    }
+  }
+  h->outg = job_f32(h, {"out.norm.g"}, c.ch[0]);
+  h->outb = job_f32(h, {"out.norm.b"}, c.ch[0]);
+  h->conv_out = conv3(h, "out.conv", c.ch[0], c.latent_c, c.ch[0]);
+  h->tb_total = tb;
+  std::vector<std::string> wn, bn;
+  for (auto& n : temb) {
+    wn.push_back(n + ".w");
+    bn.push_back(n + ".b");
+  }
+  h->tbw = job_act(h, wn, (size_t)tb * td);
+  h->tbb = job_f32(h, bn, tb);
+}
+
+// ------------------------------------------------------------- profiling
+enum Kind { K_GEMM, K_ATTN, K_GN, K_LN, K_GEGLU, K_TIME, K_PACK, K_CFG, K_COPY, K_COUNT };
+static const char* kKindName[K_COUNT] = {"gemm", "attention", "groupnorm", "layernorm", "geglu",
+                                         "time_mlp", "pack", "cfg_ddim", "copy"};
+
+static hipEvent_t take_event(sd_unet* h) {
+  if (!h->pool.empty()) {
+    hipEvent_t e = h->pool.back();
+    h->pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+static void prof_mark(sd_unet* h, int kind, double flops, double bytes, hipStream_t s) {
+  hipEvent_t e = take_event(h);
+  if (!e) return;
+  if (hipEventRecord(e, s) != hipSuccess) {
+    h->pool.push_back(e);
+    return;
+  }
+  h->recs.push_back(sd_unet::Rec{kind, flops, bytes, e});
+}
+static hipError_t prof_fold(sd_unet* h) {
+  if (h->recs.empty()) return hipSuccess;
+  hipError_t err = hipEventSynchronize(h->recs.back().ev);
+  for (size_t i = 1; i < h->recs.size() && err == hipSuccess; ++i) {
+    const auto& r = h->recs[i];
+    if (r.kind < 0) continue;
+    float ms = 0.f;
+    err = hipEventElapsedTime(&ms, h->recs[i - 1].ev, r.ev);
+    auto& t = h->tot[r.kind];
+    t.launches++;
+    t.ms += ms;
+    t.flops += r.flops;
+    t.bytes += r.bytes;
+  }
+  for (auto& r : h->recs) h->pool.push_back(r.ev);
+  h->recs.clear();
+  return err;
+}
+
+// ------------------------------------------------------------- the step
+struct Step {
+  sd_unet* h;
+  bool dry;
+  hipStream_t s;
+  int n_req, rows;
+  hipError_t err = hipSuccess;
+  const char* where = "";
+
+  void* buf(int role, size_t bytes) {
+    if (dry) {
+      size_t& n = h->need[role];
+      n = std::max(n, bytes);
+      return nullptr;
+    }
+    return h->ws + h->off.at(role);
+  }
+  const uint8_t* W(size_t off) const { return h->wdev + off; }
+  const float* Wf(size_t off) const { return reinterpret_cast<const float*>(h->wdev + off); }
+  bool ok(hipError_t e, const char* w, int kind = K_COPY, double flops = 0, double bytes = 0) {
+    if (e != hipSuccess && err == hipSuccess) {
+      err = e;
+      where = w;
+    }
+    if (err == hipSuccess && h->prof) prof_mark(h, kind, flops, bytes, s);
+    return err == hipSuccess;
+  }
+  void* at(void* p, long elems) const { return p ? (uint8_t*)p + elems * h->esz : nullptr; }
+
+  // GroupNorm statistics of [src0 | src1] -> (scale, shift) per (row, channel).
+  void gn(const void* s0, int c0, const void* s1, int c1, int hw, float eps, size_t g, size_t b,
+          float** sc, float** sh) {
+    const int cin = c0 + c1;
+    float* part = (float*)buf(R_GNP, groupnorm_partial_floats(rows, hw, cin) * 4);
+    *sc = (float*)buf(R_GNS, (size_t)rows * cin * 4);
+    *sh = (float*)buf(R_GNH, (size_t)rows * cin * 4);
+    if (dry || err) return;
+    ok(launch_groupnorm_stats(h->dt, s0, c0, s1, c1, rows, hw, h->cfg.gn_groups, eps, Wf(g), Wf(b), part,
+                              *sc, *sh, s),
+       "groupnorm", K_GN, 3.0 * rows * hw * cin, (double)rows * hw * cin * h->esz + 8.0 * rows * cin);
+  }
+
+  static ASeg seg(const void* s0, int c0, const void* s1, int c1, int ks, int stride, int up, int Hi,
+                  int Wi, const float* sc, const float* sh, int silu) {
+    ASeg a;
+    a.src0 = s0;
+    a.src1 = s1;
+    a.scale = sc;
+    a.shift = sh;
+    a.c0 = c0;
+    a.c1 = c1;
+    a.cin = c0 + c1;
+    a.ks = ks;
+    a.stride = stride;
+    a.up = up;
+    a.Hi = Hi;
+    a.Wi = Wi;
+    a.Ho = up ? 2 * Hi : (stride == 2 ? (Hi - 1) / 2 + 1 : Hi);
+    a.Wo = up ? 2 * Wi : (stride == 2 ? (Wi - 1) / 2 + 1 : Wi);
+    a.K = ks * ks * a.cin;
+    a.silu = silu;
+    return a;
+  }
+  static ASeg lin(const void* x, int K, long M) { return seg(x, K, nullptr, 0, 1, 1, 0, 1, (int)M, nullptr, nullptr, 0); }
+  static Epi epi(void* out, int ldo, const float* bias, const void* resid = nullptr, int ldr = 0) {
+    Epi e;
+    memset(&e, 0, sizeof(e));
+    e.out = out;
+    e.ldo = ldo;
+    e.bias = bias;
+    e.resid = resid;
+    e.ldr = ldr;
+    e.hw = 1;
+    return e;
+  }
+  // M defaults to rows * Ho * Wo (convolutions); linears pass it.  kalg
+  // overrides the algorithmic K (conv_in's channel padding is not counted).
+  void gemm(const ASeg& s0, const ASeg* s1, const void* B, int N, const Epi& e, const char* w, long M = -1,
+            double kalg = -1) {
+    if (dry || err) return;
+    GemmArgs a;
+    memset(&a, 0, sizeof(a));
+    a.seg[0] = s0;
+    if (s1) a.seg[1] = *s1;
+    a.M = (int)(M >= 0 ? M : (long)rows * s0.Ho * s0.Wo);
+    a.N = N;
+    a.K = s0.K + (s1 ? s1->K : 0);
+    a.B = B;
+    a.ldb = a.K;
+    a.epi = e;
+    const double K = kalg > 0 ? kalg : a.K;
+    const double es = h->esz, outb = e.out_f32 ? 4 : es;
+    auto seg_bytes = [&](const ASeg& g, long m) {
+      return (g.Hi == 1 && g.Ho == 1) ? (double)m * g.cin * es : (double)rows * g.Hi * g.Wi * g.cin * es;
+    };
+    double bytes = seg_bytes(s0, a.M) + (s1 ? seg_bytes(*s1, a.M) : 0.0) + (double)N * a.K * es +
+                   (double)a.M * N * outb + (e.resid ? (double)a.M * N * es : 0.0);
+    ok(launch_gemm(h->dt, a, s), w, K_GEMM, 2.0 * a.M * N * K, bytes);
+  }
+  // ResBlock on [src0 | src1] (H x W) -> out (cout channels).
+  void resblock(const ResW& r, const void* s0, int c0, const void* s1, int c1, int H, int W_, void* out,
+                const float* tb) {
+    const int hw = H * W_;
+    float *sc, *sh;
+    gn(s0, c0, s1, c1, hw, 1e-5f, r.n1g, r.n1b, &sc, &sh);
+    void* u = buf(R_U, (size_t)rows * hw * r.cout * h->esz);
+    Epi e1 = epi(u, r.cout, Wf(r.c1.b));
+    e1.tbias = tb;
+    e1.tb_ld = h->tb_total;
+    e1.tb_off = r.tb_off;
+    e1.hw = hw;
+    gemm(seg(s0, c0, s1, c1, 3, 1, 0, H, W_, sc, sh, 1), nullptr, W(r.c1.w), r.cout, e1, "conv1");
+    gn(u, r.cout, nullptr, 0, hw, 1e-5f, r.n2g, r.n2b, &sc, &sh);
+    const ASeg a2 = seg(u, r.cout, nullptr, 0, 3, 1, 0, H, W_, sc, sh, 1);
+    if (r.skip) {
+      const ASeg sk = seg(s0, c0, s1, c1, 1, 1, 0, H, W_, nullptr, nullptr, 0);
+      gemm(a2, &sk, W(r.c2.w), r.cout, epi(out, r.cout, Wf(r.c2.b)), "conv2+skip");
+    } else {
+      gemm(a2, nullptr, W(r.c2.w), r.cout, epi(out, r.cout, Wf(r.c2.b), s0, r.cout), "conv2");
+    }
+  }
+
+  // Transformer2D on h (H x W x C), in place.
+  void transformer(const TxW& t, void* hbuf, int H, int W_, const void* ctx, const int* row_ctx) {
+    const int hw = H * W_, C = t.C;
+    const long T = (long)rows * hw;
+    const int L = h->cfg.ctx_len, D = h->cfg.ctx_dim;
+    float *sc, *sh;
+    gn(hbuf, C, nullptr, 0, hw, 1e-6f, t.ng, t.nb, &sc, &sh);
+    void* z = buf(R_TZ, (size_t)T * C * h->esz);
+    void* x = buf(R_TX, (size_t)T * C * h->esz);
+    void* q = buf(R_TQ, (size_t)T * 4 * C * h->esz);
+    void* f = buf(R_TF, (size_t)T * 8 * C * h->esz);
+    void* ckv = buf(R_CKV, (size_t)(n_req + 1) * L * 2 * C * h->esz);
+    gemm(seg(hbuf, C, nullptr, 0, 1, 1, 0, H, W_, sc, sh, 0), nullptr, W(t.piw), C, epi(z, C, Wf(t.pib)),
+         "proj_in");
+    for (const BlkW& b : t.blk) {
+      if (!dry && !err) ok(launch_layernorm(h->dt, z, x, T, C, Wf(b.ln1g), Wf(b.ln1b), 1e-5f, s), "ln1", K_LN, 8.0 * T * C, 2.0 * T * C * h->esz);
+      gemm(lin(x, C, T), nullptr, W(b.qkv), 3 * C, epi(q, 3 * C, nullptr), "qkv", T);
+      if (!dry && !err) {
+        AttnArgs a;
+        a.q = q; a.q_ld = 3 * C; a.q_img = (long)hw * 3 * C;
+        a.k = at(q, C); a.v = at(q, 2 * C); a.kv_ld = 3 * C; a.kv_img = (long)hw * 3 * C;
+        a.kv_index = nullptr;
+        a.o = x; a.o_ld = C; a.o_img = (long)hw * C;
+        a.imgs = rows; a.heads = t.heads; a.d = t.d; a.Nq = hw; a.Nk = hw;
+        a.scale = 1.0f / sqrtf((float)t.d);
+        ok(launch_attention(h->dt, a, s), "self-attention", K_ATTN, 4.0 * rows * hw * (double)hw * C,
+           4.0 * T * C * h->esz);
+      }
+      gemm(lin(x, C, T), nullptr, W(b.o1w), C, epi(z, C, Wf(b.o1b), z, C), "attn1.out", T);
+      if (!dry && !err) ok(launch_layernorm(h->dt, z, x, T, C, Wf(b.ln2g), Wf(b.ln2b), 1e-5f, s), "ln2", K_LN, 8.0 * T * C, 2.0 * T * C * h->esz);
+      gemm(lin(x, C, T), nullptr, W(b.q2), C, epi(q, C, nullptr), "attn2.q", T);
+      gemm(lin(ctx, D, (long)(n_req + 1) * L), nullptr, W(b.kv2), 2 * C, epi(ckv, 2 * C, nullptr), "attn2.kv",
+           (long)(n_req + 1) * L);
+      if (!dry && !err) {
+        AttnArgs a;
+        a.q = q; a.q_ld = C; a.q_img = (long)hw * C;
+        a.k = ckv; a.v = at(ckv, C); a.kv_ld = 2 * C; a.kv_img = (long)L * 2 * C;
+        a.kv_index = row_ctx;
+        a.o = x; a.o_ld = C; a.o_img = (long)hw * C;
+        a.imgs = rows; a.heads = t.heads; a.d = t.d; a.Nq = hw; a.Nk = L;
+        a.scale = 1.0f / sqrtf((float)t.d);
+        ok(launch_attention(h->dt, a, s), "cross-attention", K_ATTN, 4.0 * rows * hw * (double)L * C,
+           (2.0 * T * C + 2.0 * (n_req + 1) * L * C) * h->esz);
+      }
+      gemm(lin(x, C, T), nullptr, W(b.o2w), C, epi(z, C, Wf(b.o2b), z, C), "attn2.out", T);
+      if (!dry && !err) ok(launch_layernorm(h->dt, z, x, T, C, Wf(b.ln3g), Wf(b.ln3b), 1e-5f, s), "ln3", K_LN, 8.0 * T * C, 2.0 * T * C * h->esz);
+      gemm(lin(x, C, T), nullptr, W(b.f1w), 8 * C, epi(f, 8 * C, Wf(b.f1b)), "ff1", T);
+      if (!dry && !err) ok(launch_geglu(h->dt, f, q, T, 4 * C, s), "geglu", K_GEGLU, 4.0 * T * 4 * C, 12.0 * T * C * h->esz);
+      gemm(lin(q, 4 * C, T), nullptr, W(b.f2w), C, epi(z, C, Wf(b.f2b), z, C), "ff2", T);
+    }
+    gemm(lin(z, C, T), nullptr, W(t.pow), C, epi(hbuf, C, Wf(t.pob), hbuf, C), "proj_out", T);
+  }
+
+  void run(const float* lat_in, const void* ctx_c, const void* ctx_u, const float* pool_c,
+           const float* pool_u, float* lat_out, float* eps_out) {
+    const sd_unet_config& c = h->cfg;
+    const int nl = c.n_levels, td = c.temb_dim;
+    int H = c.latent_h, Wd = c.latent_w;
+    const int L = c.ctx_len, D = c.ctx_dim;
+    // per-step scalars (uploaded by the caller of run)
+    uint8_t* scal = (uint8_t*)buf(R_SCAL, h->scal_bytes);
+    const int R = c.max_requests;
+    const int* row_req = (const int*)(scal);
+    const int* row_branch = (const int*)(scal + 4 * (2 * R));
+    const int* row_ctx = (const int*)(scal + 4 * (4 * R));
+    const float* row_t = (const float*)(scal + 4 * (6 * R));
+    const int* req_row_u = (const int*)(scal + 4 * (8 * R));
+    const float* req_coef = (const float*)(scal + 4 * (9 * R));
+    const float* time_ids = (const float*)(scal + 4 * (12 * R));
+
+    if (!dry && h->prof) prof_mark(h, -1, 0, 0, s);
+    // contexts: [cond_0 .. cond_{n-1}, uncond]
+    void* ctx = buf(R_CTX, (size_t)(n_req + 1) * L * D * h->esz);
+    if (!dry && !err) {
+      const size_t one = (size_t)L * D * h->esz;
+      ok(hipMemcpyAsync(ctx, ctx_c, one * n_req, hipMemcpyDeviceToDevice, s), "ctx copy", K_COPY, 0, 2.0 * one * n_req);
+      if (ctx_u) ok(hipMemcpyAsync((uint8_t*)ctx + one * n_req, ctx_u, one, hipMemcpyDeviceToDevice, s), "ctx copy", K_COPY, 0, 2.0 * one);
+    }
+    // time embedding -> per-row time bias of every ResBlock
+    float* e = (float*)buf(R_E, (size_t)rows * c.temb_in * 4);
+    float* a = c.add_in ? (float*)buf(R_A, (size_t)rows * c.add_in * 4) : nullptr;
+    float* h1 = (float*)buf(R_H1, (size_t)rows * td * 4);
+    float* tau = (float*)buf(R_TAU, (size_t)rows * td * 4);
+    float* t2 = c.add_in ? (float*)buf(R_T2, (size_t)rows * td * 4) : nullptr;
+    float* tb = (float*)buf(R_TB, (size_t)rows * h->tb_total * 4);
+    if (!dry && !err) {
+      ok(launch_time_inputs(row_t, rows, c.temb_in, e, pool_c, pool_u, row_req, row_branch, c.pooled_dim,
+                            time_ids, c.n_time_ids, c.time_id_dim, a, s),
+         "time inputs", K_TIME, 0, 4.0 * rows * (c.temb_in + c.add_in));
+      ok(launch_linear_smallm(h->dt, e, rows, c.temb_in, W(h->t1w), Wf(h->t1b), nullptr, h1, td, 0, 1, s), "time.lin1", K_TIME,
+         2.0 * rows * td * c.temb_in, (double)td * c.temb_in * h->esz);
+      ok(launch_linear_smallm(h->dt, h1, rows, td, W(h->t2w), Wf(h->t2b), nullptr, tau, td, 0, 0, s), "time.lin2", K_TIME,
+         2.0 * rows * td * td, (double)td * td * h->esz);
+      if (c.add_in) {
+        ok(launch_linear_smallm(h->dt, a, rows, c.add_in, W(h->a1w), Wf(h->a1b), nullptr, t2, td, 0, 1, s), "add.lin1", K_TIME,
+           2.0 * rows * td * c.add_in, (double)td * c.add_in * h->esz);
+        ok(launch_linear_smallm(h->dt, t2, rows, td, W(h->a2w), Wf(h->a2b), tau, tau, td, 0, 0, s), "add.lin2", K_TIME,
+           2.0 * rows * td * td, (double)td * td * h->esz);
+      }
+      ok(launch_linear_smallm(h->dt, tau, rows, td, W(h->tbw), Wf(h->tbb), nullptr, tb, h->tb_total, 1, 0, s), "temb",
+         K_TIME, 2.0 * rows * td * h->tb_total, (double)td * h->tb_total * h->esz + 4.0 * rows * h->tb_total);
+    }
+    // pack + conv_in
+    void* x0 = buf(R_X0, (size_t)rows * H * Wd * h->cpad * h->esz);
+    if (!dry && !err)
+      ok(launch_pack_latents(h->dt, lat_in, x0, rows, c.latent_c, H * Wd, h->cpad, row_req, s), "pack", K_PACK, 0,
+         4.0 * n_req * c.latent_c * H * Wd + (double)rows * H * Wd * h->cpad * h->esz);
+    std::vector<void*> skip(h->n_skips);
+    std::vector<int> skipc(h->n_skips);
+    int k = 0;
+    auto skipbuf = [&](int ch, int hh, int ww) {
+      skipc[k] = ch;
+      skip[k] = buf(R_SKIP0 + k, (size_t)rows * hh * ww * ch * h->esz);
+      return skip[k++];
+    };
+    void* cur = skipbuf(c.ch[0], H, Wd);
+    gemm(seg(x0, h->cpad, nullptr, 0, 3, 1, 0, H, Wd, nullptr, nullptr, 0), nullptr, W(h->conv_in.w), c.ch[0],
+         epi(cur, c.ch[0], Wf(h->conv_in.b)), "conv_in", -1, 9.0 * c.latent_c);
+    int curc = c.ch[0];
+    for (int l = 0; l < nl; ++l) {
+      const LevelW& lv = h->down[l];
+      for (int i = 0; i < c.n_res; ++i) {
+        const ResW& r = lv.res[i];
+        void* o = skipbuf(r.cout, H, Wd);
+        resblock(r, cur, curc, nullptr, 0, H, Wd, o, tb);
+        if (!lv.tx.empty()) transformer(lv.tx[i], o, H, Wd, ctx, row_ctx);
+        cur = o;
+        curc = r.cout;
+      }
+      if (lv.has_conv) {
+        const int Ho = H / 2, Wo = Wd / 2;
+        void* o = skipbuf(curc, Ho, Wo);
+        gemm(seg(cur, curc, nullptr, 0, 3, 2, 0, H, Wd, nullptr, nullptr, 0), nullptr, W(lv.conv.w), curc,
+             epi(o, curc, Wf(lv.conv.b)), "downsample");
+        cur = o;
+        H = Ho;
+        Wd = Wo;
+      }
+    }
+    // hidden ping-pong buffers
+    auto hbuf = [&](int role, int ch, int hh, int ww) { return buf(role, (size_t)rows * hh * ww * ch * h->esz); };
+    void* ha = hbuf(R_HA, curc, H, Wd);
+    resblock(h->mid0, cur, curc, nullptr, 0, H, Wd, ha, tb);
+    if (!h->midtx.empty()) transformer(h->midtx[0], ha, H, Wd, ctx, row_ctx);
+    void* hb = hbuf(R_HB, curc, H, Wd);
+    resblock(h->mid1, ha, curc, nullptr, 0, H, Wd, hb, tb);
+    cur = hb;
+    int cur_role = R_HB;
+    for (int l = nl - 1; l >= 0; --l) {
+      const LevelW& lv = h->up[l];
+      for (int i = 0; i <= c.n_res; ++i) {
+        const ResW& r = lv.res[i];
+        --k;
+        const int nrole = cur_role == R_HA ? R_HB : R_HA;
+        void* o = hbuf(nrole, r.cout, H, Wd);
+        resblock(r, cur, curc, skip[k], skipc[k], H, Wd, o, tb);
+        if (!lv.tx.empty()) transformer(lv.tx[i], o, H, Wd, ctx, row_ctx);
+        cur = o;
+        cur_role = nrole;
+        curc = r.cout;
+      }
+      if (lv.has_conv) {
+        const int nrole = cur_role == R_HA ? R_HB : R_HA;
+        void* o = hbuf(nrole, curc, 2 * H, 2 * Wd);
+        gemm(seg(cur, curc, nullptr, 0, 3, 1, 1, H, Wd, nullptr, nullptr, 0), nullptr, W(lv.conv.w), curc,
+             epi(o, curc, Wf(lv.conv.b)), "upsample");
+        cur = o;
+        cur_role = nrole;
+        H *= 2;
+        Wd *= 2;
+      }
+    }
+    // output: GN + SiLU + conv (fp32 eps rows), then CFG combine + DDIM
+    float *sc, *sh;
+    gn(cur, curc, nullptr, 0, H * Wd, 1e-5f, h->outg, h->outb, &sc, &sh);
+    float* eps = (float*)buf(R_EPS, (size_t)rows * H * Wd * c.latent_c * 4);
+    Epi eo = epi(eps, c.latent_c, Wf(h->conv_out.b));
+    eo.out_f32 = 1;
+    gemm(seg(cur, curc, nullptr, 0, 3, 1, 0, H, Wd, sc, sh, 1), nullptr, W(h->conv_out.w), c.latent_c, eo, "conv_out");
+    if (!dry && !err)
+      ok(launch_cfg_ddim(eps, lat_in, lat_out, eps_out, n_req, c.latent_c, H * Wd, req_row_u, req_coef, s),
+         "cfg+ddim", K_CFG, 4.0 * n_req * c.latent_c * H * Wd,
+         4.0 * c.latent_c * H * Wd * (rows + 2.0 * n_req + (eps_out ? n_req : 0)));
+  }
+};
+
+static void plan_workspace(sd_unet* h) {
+  const int R = h->cfg.max_requests;
+  h->scal_bytes = (size_t)4 * (12 * R + 64);
+  Step st{h, true, nullptr, R, 2 * R};
+  st.run(nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
+  size_t o = 0;
+  for (auto& kv : h->need) {
+    h->off[kv.first] = o;
+    o = align256(o + kv.second);
+  }
+  h->wsbytes = o;
+}
+
+static bool get_config(const sd_unet_config* cfg, std::string& why) {
+  if (!cfg) {
+    why = "cfg is NULL";
+    return false;
+  }
+  why = check_config(*cfg);
+  return why.empty();
+}
+
+// Build a handle skeleton (layout + workspace plan) without device buffers.
+static sd_unet* skeleton(const sd_unet_config* cfg) {
+  sd_unet* h = new sd_unet();
+  h->cfg = *cfg;
+  h->dt = cfg->dtype == SD_BF16 ? BF16 : F32;
+  h->esz = cfg->dtype == SD_BF16 ? 2 : 4;
+  h->manifest = build_manifest(*cfg);
+  build_layout(h);
+  plan_workspace(h);
+  return h;
+}
+
+static bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb) {
+  const uint8_t *pa = (const uint8_t*)a, *pb = (const uint8_t*)b;
+  return pa < pb + nb && pb < pa + na;
+}
+
+}  // namespace sd
+
+using namespace sd;
+
+extern "C" {
+
+int32_t synerdiff_abi_version(void) { return SYNERDIFF_ABI_VERSION; }
+
+const char* synerdiff_last_error(void) { return g_err.c_str(); }
+
+sd_status synerdiff_config_check(const sd_unet_config* cfg) {
+  std::string why;
+  if (!cfg) return fail(SD_ERR_INVALID_ARG, "cfg is NULL");
+  if (!get_config(cfg, why)) return fail(SD_ERR_UNSUPPORTED, why);
+  return SD_OK;
+}
+
+int64_t synerdiff_param_count(const sd_unet_config* cfg) {
+  std::string why;
+  if (!get_config(cfg, why)) {
+    fail(SD_ERR_UNSUPPORTED, why);
+    return -1;
+  }
+  return (int64_t)build_manifest(*cfg).size();
+}
+
+sd_status synerdiff_param_info(const sd_unet_config* cfg, int64_t i, char* name, size_t name_cap,
+                               int64_t shape[4], int32_t* ndim) {
+  std::string why;
+  if (!get_config(cfg, why)) return fail(SD_ERR_UNSUPPORTED, why);
+  if (!name || name_cap == 0 || !shape || !ndim) return fail(SD_ERR_INVALID_ARG, "NULL output pointer");
+  const auto m = build_manifest(*cfg);
+  if (i < 0 || i >= (int64_t)m.size()) return fail(SD_ERR_INVALID_ARG, "parameter index out of range");
+  const Param& p = m[(size_t)i];
+  const size_t n = std::min(name_cap - 1, p.name.size());
+  memcpy(name, p.name.data(), n);
+  name[n] = 0;
+  *ndim = (int32_t)p.shape.size();
+  for (int k = 0; k < 4; ++k) shape[k] = k < (int)p.shape.size() ? p.shape[k] : 1;
+  return SD_OK;
+}
+
+size_t synerdiff_weights_bytes(const sd_unet_config* cfg) {
+  std::string why;
+  if (!get_config(cfg, why)) return 0;
+  sd_unet* h = skeleton(cfg);
+  const size_t n = align256(h->wtotal);
+  delete h;
+  return n;
+}
+
+size_t synerdiff_workspace_bytes(const sd_unet_config* cfg) {
+  std::string why;
+  if (!get_config(cfg, why)) return 0;
+  sd_unet* h = skeleton(cfg);
+  const size_t n = h->wsbytes;
+  delete h;
+  return n;
+}
+
+sd_status synerdiff_unet_create(const sd_unet_config* cfg, void* d_weights, size_t weights_bytes,
+                                void* d_workspace, size_t workspace_bytes, sd_unet** out) {
+  std::string why;
+  if (!out) return fail(SD_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (!cfg) return fail(SD_ERR_INVALID_ARG, "cfg is NULL");
+  if (!get_config(cfg, why)) return fail(SD_ERR_UNSUPPORTED, why);
+  if (!d_weights || !d_workspace) return fail(SD_ERR_INVALID_ARG, "NULL device buffer");
+  if (((uintptr_t)d_weights & 255) || ((uintptr_t)d_workspace & 255))
+    return fail(SD_ERR_INVALID_ARG, "device buffers must be 256-byte aligned");
+  sd_unet* h = skeleton(cfg);
+  if (weights_bytes < align256(h->wtotal) || workspace_bytes < h->wsbytes) {
+    delete h;
+    return fail(SD_ERR_WORKSPACE, "weight or workspace buffer too small");
+  }
+  h->wdev = (uint8_t*)d_weights;
+  h->wbytes = weights_bytes;
+  h->ws = (uint8_t*)d_workspace;
+  *out = h;
+  return SD_OK;
+}
+
+// The pinned staging ring and its events are created on the first step, so
+// that creating a handle makes no HIP call.
+static sd_status ensure_staging(sd_unet* h) {
+  if (h->pinned) return SD_OK;
+  if (hipHostMalloc((void**)&h->pinned, h->scal_bytes * sd_unet::SLOTS, hipHostMallocDefault) != hipSuccess) {
+    h->pinned = nullptr;
+    return fail(SD_ERR_HIP, "hipHostMalloc failed");
+  }
+  for (int i = 0; i < sd_unet::SLOTS; ++i)
+    if (hipEventCreateWithFlags(&h->ev[i], hipEventDisableTiming) != hipSuccess)
+      return fail(SD_ERR_HIP, "hipEventCreate failed");
+  return SD_OK;
+}
+
+void synerdiff_unet_destroy(sd_unet* h) {
+  if (!h) return;
+  (void)prof_fold(h);
+  for (hipEvent_t e : h->pool) (void)hipEventDestroy(e);
+  for (int i = 0; i < sd_unet::SLOTS; ++i)
+    if (h->ev[i]) {
+      (void)hipEventSynchronize(h->ev[i]);
+      (void)hipEventDestroy(h->ev[i]);
+    }
+  if (h->pinned) (void)hipHostFree(h->pinned);
+  delete h;
+}
+
+sd_status synerdiff_load_weights(sd_unet* h, const float* hp, size_t n_floats, void* stream) {
+  if (!h || !hp) return fail(SD_ERR_INVALID_ARG, "NULL argument");
+  const Param& last = h->manifest.back();
+  if (n_floats != last.offset + last.numel) return fail(SD_ERR_INVALID_ARG, "n_floats does not match the manifest");
+  std::map<std::string, const Param*> by;
+  for (auto& p : h->manifest) by[p.name] = &p;
+  std::vector<uint8_t> host(align256(h->wtotal), 0);
+  const bool bf = h->dt == BF16;
+  auto put_act = [&](size_t dst, size_t idx, float v) {
+    if (bf) {
+      const uint16_t b = f2bf(v);
+      memcpy(&host[dst + idx * 2], &b, 2);
+    } else {
+      memcpy(&host[dst + idx * 4], &v, 4);
+    }
+  };
+  for (const PackJob& j : h->jobs) {
+    std::vector<const Param*> src;
+    for (auto& n : j.names) {
+      auto it = by.find(n);
+      if (it == by.end()) return fail(SD_ERR_INVALID_ARG, "internal: missing parameter " + n);
+      src.push_back(it->second);
+    }
+    switch (j.kind) {
+      case P_ACT: {
+        size_t o = 0;
+        for (auto* p : src)
+          for (size_t i = 0; i < p->numel; ++i) put_act(j.dst, o++, hp[p->offset + i]);
+        break;
+      }
+      case P_F32: {
+        size_t o = 0;
+        for (auto* p : src) {
+          memcpy(&host[j.dst + o * 4], hp + p->offset, p->numel * 4);
+          o += p->numel;
+        }
+        break;
+      }
+      case P_F32_SUM: {
+        for (size_t i = 0; i < src[0]->numel; ++i) {
+          const float v = hp[src[0]->offset + i] + hp[src[1]->offset + i];
+          memcpy(&host[j.dst + i * 4], &v, 4);
+        }
+        break;
+      }
+      case P_CONV3:
+      case P_CONV3_SKIP: {
+        const Param* w = src[0];
+        const int cout = (int)w->shape[0], cin = (int)w->shape[1];
+        const int cp = j.cin_pad;
+        const int K = 9 * cp + (j.kind == P_CONV3_SKIP ? (int)src[1]->shape[1] : 0);
+        for (int o = 0; o < cout; ++o) {
+          for (int tap = 0; tap < 9; ++tap)
+            for (int c = 0; c < cp; ++c) {
+              const float v = c < cin ? hp[w->offset + ((size_t)o * cin + c) * 9 + tap] : 0.f;
+              put_act(j.dst, (size_t)o * K + tap * cp + c, v);
+            }
+          if (j.kind == P_CONV3_SKIP) {
+            const Param* s = src[1];
+            const int sc = (int)s->shape[1];
+            for (int c = 0; c < sc; ++c) put_act(j.dst, (size_t)o * K + 9 * cp + c, hp[s->offset + (size_t)o * sc + c]);
+          }
+        }
+        break;
+      }
+    }
+  }
+  hipStream_t s = (hipStream_t)stream;
+  if (hipMemcpyAsync(h->wdev, host.data(), host.size(), hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return fail(SD_ERR_HIP, "weight upload failed");
+  return SD_OK;
+}
+
+sd_status synerdiff_row_plan(int32_t n_req, const uint8_t* cfg_on, int32_t* row_req, int32_t* row_branch,
+                             int32_t* req_row_u, int32_t* n_rows) {
+  if (n_req < 0) return fail(SD_ERR_INVALID_ARG, "n_req < 0");
+  if (n_req > 0 && (!cfg_on || !row_req || !row_branch || !req_row_u)) return fail(SD_ERR_INVALID_ARG, "NULL array");
+  if (!n_rows) return fail(SD_ERR_INVALID_ARG, "n_rows is NULL");
+  for (int r = 0; r < n_req; ++r)
+    if (cfg_on[r] > 1) return fail(SD_ERR_INVALID_ARG, "cfg_on must be 0 or 1");
+  int u = n_req;
+  for (int r = 0; r < n_req; ++r) {
+    row_req[r] = r;
+    row_branch[r] = 0;
+  }
+  for (int r = 0; r < n_req; ++r) {
+    if (cfg_on[r]) {
+      row_req[u] = r;
+      row_branch[u] = 1;
+      req_row_u[r] = u++;
+    } else {
+      req_row_u[r] = -1;
+    }
+  }
+  *n_rows = u;
+  return SD_OK;
+}
+
+sd_status synerdiff_alphas_cumprod(int32_t schedule, double out[1000]) {
+  if (!out) return fail(SD_ERR_INVALID_ARG, "out is NULL");
+  double acc = 1.0;
+  for (int t = 0; t < 1000; ++t) {
+    const double s = t / 999.0;
+    double beta;
+    if (schedule == SD_SCHED_LINEAR) {
+      beta = 1e-4 + (0.02 - 1e-4) * s;
+    } else if (schedule == SD_SCHED_SCALED_LINEAR) {
+      const double a = sqrt(0.00085), b = sqrt(0.012);
+      beta = (a + (b - a) * s) * (a + (b - a) * s);
+    } else {
+      return fail(SD_ERR_INVALID_ARG, "unknown schedule");
+    }
+    acc *= 1.0 - beta;
+    out[t] = acc;
+  }
+  return SD_OK;
+}
+
+sd_status synerdiff_ddim_coef(const double* ac, int32_t t, int32_t t_prev, float out_AB[2]) {
+  if (!ac || !out_AB) return fail(SD_ERR_INVALID_ARG, "NULL argument");
+  if (t < 0 || t > 999 || t_prev > 999 || t_prev >= t) return fail(SD_ERR_INVALID_ARG, "need 0 <= t_prev < t <= 999 or t_prev < 0");
+  const double at = ac[t], ap = t_prev < 0 ? 1.0 : ac[t_prev];
+  out_AB[0] = (float)sqrt(ap / at);
+  out_AB[1] = (float)(sqrt(1.0 - ap) - sqrt(ap * (1.0 - at) / at));
+  return SD_OK;
+}
+
+sd_status synerdiff_unet_step(sd_unet* h, int32_t n_req, const float* lat_in, const int32_t* ts,
+                              const uint8_t* cfg_on, const float* guidance, const void* ctx_c,
+                              const void* ctx_u, const float* pool_c, const float* pool_u,
+                              const float* time_ids, const float* coef, float* lat_out, float* eps_out,
+                              void* stream) {
+  if (!h) return fail(SD_ERR_INVALID_ARG, "handle is NULL");
+  if (n_req < 0) return fail(SD_ERR_INVALID_ARG, "n_req < 0");
+  if (n_req == 0) return SD_OK;
+  const sd_unet_config& c = h->cfg;
+  if (n_req > c.max_requests) return fail(SD_ERR_CAPACITY, "n_req exceeds max_requests");
+  if (!lat_in || !ts || !cfg_on || !ctx_c || !coef || !lat_out) return fail(SD_ERR_INVALID_ARG, "NULL argument");
+  int ncfg = 0;
+  for (int r = 0; r < n_req; ++r) {
+    if (ts[r] < 0 || ts[r] > 999) return fail(SD_ERR_INVALID_ARG, "timestep out of [0, 999]");
+    if (cfg_on[r] > 1) return fail(SD_ERR_INVALID_ARG, "cfg_on must be 0 or 1");
+    if (!std::isfinite(coef[2 * r]) || !std::isfinite(coef[2 * r + 1]))
+      return fail(SD_ERR_INVALID_ARG, "non-finite sampler coefficient");
+    if (cfg_on[r]) {
+      ++ncfg;
+      if (!guidance) return fail(SD_ERR_INVALID_ARG, "guidance is NULL");
+      if (!std::isfinite(guidance[r])) return fail(SD_ERR_INVALID_ARG, "non-finite guidance");
+    }
+  }
+  if (ncfg && !ctx_u) return fail(SD_ERR_INVALID_ARG, "ctx_uncond is NULL");
+  if (c.add_in) {
+    if (!pool_c || (ncfg && !pool_u) || (c.n_time_ids && !time_ids))
+      return fail(SD_ERR_INVALID_ARG, "pooled / time_ids required for the added embedding");
+  } else if (pool_c || pool_u) {
+    return fail(SD_ERR_INVALID_ARG, "pooled inputs given but the config has no added embedding");
+  }
+  const size_t lat_bytes = (size_t)n_req * c.latent_c * c.latent_h * c.latent_w * 4;
+  if (lat_out != lat_in && ranges_overlap(lat_out, lat_bytes, lat_in, lat_bytes))
+    return fail(SD_ERR_INVALID_ARG, "latents_out partially overlaps latents_in");
+  if (eps_out && (ranges_overlap(eps_out, lat_bytes, lat_in, lat_bytes) || ranges_overlap(eps_out, lat_bytes, lat_out, lat_bytes)))
+    return fail(SD_ERR_INVALID_ARG, "eps_out overlaps the latents");
+
+  // row plan + scalars into a pinned slot, one H2D copy
+  if (ensure_staging(h) != SD_OK) return SD_ERR_HIP;
+  const int R = c.max_requests;
+  hipStream_t s = (hipStream_t)stream;
+  const int slot = h->slot;
+  h->slot = (h->slot + 1) % sd_unet::SLOTS;
+  if (hipEventSynchronize(h->ev[slot]) != hipSuccess) return fail(SD_ERR_HIP, "staging event wait failed");
+  uint8_t* p = h->pinned + h->scal_bytes * slot;
+  memset(p, 0, h->scal_bytes);
+  int32_t* row_req = (int32_t*)p;
+  int32_t* row_branch = (int32_t*)(p + 4 * (2 * R));
+  int32_t* row_ctx = (int32_t*)(p + 4 * (4 * R));
+  float* row_t = (float*)(p + 4 * (6 * R));
+  int32_t* req_row_u = (int32_t*)(p + 4 * (8 * R));
+  float* req_coef = (float*)(p + 4 * (9 * R));
+  float* tid = (float*)(p + 4 * (12 * R));
+  int rows = 0;
+  synerdiff_row_plan(n_req, cfg_on, row_req, row_branch, req_row_u, &rows);
+  for (int i = 0; i < rows; ++i) {
+    row_ctx[i] = row_branch[i] ? n_req : row_req[i];
+    row_t[i] = (float)ts[row_req[i]];
+  }
+  for (int r = 0; r < n_req; ++r) {
+    req_coef[3 * r] = coef[2 * r];
+    req_coef[3 * r + 1] = coef[2 * r + 1];
+    req_coef[3 * r + 2] = cfg_on[r] ? guidance[r] : 1.0f;
+  }
+  for (int i = 0; i < c.n_time_ids && time_ids; ++i) tid[i] = time_ids[i];
+  if (hipMemcpyAsync(h->ws + h->off.at(R_SCAL), p, h->scal_bytes, hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipEventRecord(h->ev[slot], s) != hipSuccess)
+    return fail(SD_ERR_HIP, "scalar upload failed");
+
+  Step st{h, false, s, n_req, rows};
+  st.run(lat_in, ctx_c, ctx_u, pool_c, pool_u, lat_out, eps_out);
+  if (st.err != hipSuccess)
+    return fail(SD_ERR_HIP, std::string("HIP error in ") + st.where + ": " + hipGetErrorString(st.err));
+  return SD_OK;
+}
+
+sd_status synerdiff_profile(sd_unet* h, int32_t enable) {
+  if (!h) return fail(SD_ERR_INVALID_ARG, "handle is NULL");
+  h->prof = enable != 0;
+  return SD_OK;
+}
+
+sd_status synerdiff_profile_read(sd_unet* h, sd_kernel_stat* out, int32_t cap, int32_t* n_out, int32_t reset) {
+  if (!h || !n_out || (cap > 0 && !out)) return fail(SD_ERR_INVALID_ARG, "NULL argument");
+  if (prof_fold(h) != hipSuccess) return fail(SD_ERR_HIP, "profiling event query failed");
+  int n = 0;
+  for (int k = 0; k < K_COUNT; ++k) {
+    if (!h->tot[k].launches) continue;
+    if (n < cap) {
+      sd_kernel_stat& o = out[n];
+      memset(&o, 0, sizeof(o));
+      strncpy(o.name, kKindName[k], sizeof(o.name) - 1);
+      o.launches = h->tot[k].launches;
+      o.ms = h->tot[k].ms;
+      o.flop = h->tot[k].flops;
+      o.bytes = h->tot[k].bytes;
+    }
+    ++n;
+  }
+  *n_out = n;
+  if (reset)
+    for (auto& t : h->tot) t = sd_unet::Tot();
+  return SD_OK;
+}
+
+}  // extern "C"

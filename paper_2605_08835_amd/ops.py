@@ -1,0 +1,65 @@
+"""Python wrappers of the kernel-level entry points (include/synerdiff_ops.h).
+Tensors are torch device tensors; activations channels-last."""
+import torch
+
+from .binding import SD_BF16, SD_F32, _check, _ptr, lib
+
+
+def _dt(t):
+    if t.dtype == torch.bfloat16:
+        return SD_BF16
+    if t.dtype == torch.float32:
+        return SD_F32
+    raise TypeError(t.dtype)
+
+
+def _s():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def conv(x0, w_packed, cout, ks=3, stride=1, up=0, x1=None, scale=None, shift=None, silu=0, bias=None,
+         resid=None, out=None, out_f32=False):
+    n, H, W, c0 = x0.shape
+    c1 = 0 if x1 is None else x1.shape[3]
+    Ho, Wo = (2 * H, 2 * W) if up else (H // stride, W // stride)
+    if out is None:
+        out = torch.empty(n, Ho, Wo, cout, device=x0.device, dtype=torch.float32 if out_f32 else x0.dtype)
+    _check(lib().synerdiff_op_conv(_dt(x0), _ptr(x0), c0, _ptr(x1), c1, n, H, W, ks, stride, up, _ptr(scale),
+                                   _ptr(shift), silu, _ptr(w_packed), cout, _ptr(bias), _ptr(resid), _ptr(out),
+                                   int(out_f32), _s()))
+    return out
+
+
+def attention(q, k, v, o, n, heads, d, n_q, n_k, q_ld, kv_ld, o_ld, q_img, kv_img, o_img, scale,
+              kv_index=None):
+    _check(lib().synerdiff_op_attention(_dt(q), _ptr(q), q_ld, q_img, _ptr(k), _ptr(v), kv_ld, kv_img,
+                                        _ptr(kv_index), _ptr(o), o_ld, o_img, n, heads, d, n_q, n_k,
+                                        float(scale), _s()))
+    return o
+
+
+def groupnorm_stats(x0, groups, eps, gamma, beta, x1=None):
+    n, H, W, c0 = x0.shape
+    c1 = 0 if x1 is None else x1.shape[3]
+    cin = c0 + c1
+    part = torch.empty(lib().synerdiff_op_groupnorm_scratch_floats(n, H * W, cin), device=x0.device)
+    scale = torch.empty(n, cin, device=x0.device)
+    shift = torch.empty(n, cin, device=x0.device)
+    _check(lib().synerdiff_op_groupnorm_stats(_dt(x0), _ptr(x0), c0, _ptr(x1), c1, n, H * W, groups, float(eps),
+                                              _ptr(gamma), _ptr(beta), _ptr(part), _ptr(scale), _ptr(shift), _s()))
+    return scale, shift
+
+
+def layernorm(x, gamma, beta, eps=1e-5):
+    y = torch.empty_like(x)
+    C = x.shape[-1]
+    _check(lib().synerdiff_op_layernorm(_dt(x), _ptr(x), _ptr(y), x.numel() // C, C, _ptr(gamma), _ptr(beta),
+                                        float(eps), _s()))
+    return y
+
+
+def geglu(x):
+    half = x.shape[-1] // 2
+    y = torch.empty(x.shape[:-1] + (half,), device=x.device, dtype=x.dtype)
+    _check(lib().synerdiff_op_geglu(_dt(x), _ptr(x), _ptr(y), x.numel() // x.shape[-1], half, _s()))
+    return y

@@ -1,0 +1,168 @@
+"""Kernel-level parity on the GPU: each kernel of the step against the
+oracle's layer function on the same (bf16-representable) inputs."""
+import math
+
+import numpy as np
+import pytest
+
+from fixtures import bf16_round
+from oracle import ops as O
+from tests.gpu_util import log, rel_l2
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+TOL = {"f32": 2e-6, "bf16": 1.2e-2}
+
+
+def _tdt(dt):
+    return torch.bfloat16 if dt == "bf16" else torch.float32
+
+
+def _vals(rng, shape, dt, scale=1.0):
+    x = (rng.standard_normal(shape) * scale).astype(np.float32)
+    return bf16_round(x) if dt == "bf16" else x
+
+
+def _dev(x, dt=None):
+    t = torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    return t.to(_tdt(dt)) if dt else t
+
+
+@pytest.fixture(scope="module")
+def ops():
+    from paper_2605_08835_amd import ops as P
+    return P
+
+
+def _pack(w):
+    cout, cin, k, _ = w.shape
+    return np.ascontiguousarray(w.transpose(0, 2, 3, 1).reshape(cout, k * k * cin))
+
+
+CONV_CASES = [
+    # n, H, W, c0, c1, cout, ks, stride, up, affine
+    (2, 12, 10, 64, 0, 96, 3, 1, 0, False),
+    (3, 8, 8, 32, 48, 64, 3, 1, 0, True),
+    (2, 16, 16, 64, 0, 64, 3, 2, 0, False),
+    (2, 6, 5, 64, 0, 128, 3, 1, 1, False),
+    (2, 9, 7, 40, 24, 136, 1, 1, 0, False),
+    (1, 20, 20, 8, 0, 320, 3, 1, 0, False),
+    (3, 8, 8, 320, 0, 4, 3, 1, 0, True),
+]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("case", CONV_CASES)
+def test_conv(ops, dt, case):
+    n, H, W, c0, c1, cout, ks, stride, up, aff = case
+    log(f"conv {dt} {case}")
+    rng = np.random.default_rng(hash(case) % 2**32)
+    x0 = _vals(rng, (n, H, W, c0), dt)
+    x1 = _vals(rng, (n, H, W, c1), dt) if c1 else None
+    w = _vals(rng, (cout, c0 + c1, ks, ks), dt, 1.0 / math.sqrt(ks * ks * (c0 + c1)))
+    b = rng.standard_normal(cout).astype(np.float32)
+    Ho, Wo = (2 * H, 2 * W) if up else (H // stride, W // stride)
+    res = _vals(rng, (n, Ho, Wo, cout), dt)
+    scale = shift = None
+    if aff:
+        scale = (1 + 0.3 * rng.standard_normal((n, c0 + c1))).astype(np.float32)
+        shift = (0.3 * rng.standard_normal((n, c0 + c1))).astype(np.float32)
+    out_f32 = cout == 4
+    got = ops.conv(_dev(x0, dt), _dev(_pack(w), dt), cout, ks, stride, up,
+                   x1=_dev(x1, dt) if c1 else None,
+                   scale=_dev(scale) if aff else None, shift=_dev(shift) if aff else None, silu=int(aff),
+                   bias=_dev(b), resid=None if out_f32 else _dev(res, dt), out_f32=out_f32)
+    torch.cuda.synchronize()
+    got = got.float().cpu().numpy()
+    for i in range(n):
+        a = x0[i].astype(np.float64) if not c1 else np.concatenate([x0[i], x1[i]], axis=2).astype(np.float64)
+        if aff:
+            a = O.silu(a * scale[i] + shift[i])
+        if up:
+            a = O.upsample_nearest2x(a)
+        ref = O.conv2d(a, w, b, stride) + (0 if out_f32 else res[i])
+        err = rel_l2(got[i], ref)
+        assert err <= TOL[dt], (i, err)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("heads,d,nq,nk,scale,cross", [
+    (2, 8, 70, 70, 1.0, False), (2, 16, 33, 8, 1.0, True), (4, 32, 200, 200, 1.0, False),
+    (8, 40, 300, 300, 1.0, False), (8, 40, 129, 77, 1.0, True), (2, 64, 256, 256, 30.0, False),
+    (8, 80, 160, 160, 1.0, False), (8, 160, 64, 64, 1.0, False), (8, 160, 90, 77, 1.0, True),
+])
+def test_attention(ops, dt, heads, d, nq, nk, scale, cross):
+    if dt == "f32" and d > 64:
+        pytest.skip("fp32 attention covers head widths <= 64")
+    log(f"attention {dt} heads={heads} d={d} nq={nq} nk={nk} x{scale} cross={cross}")
+    rng = np.random.default_rng(d * 1000 + nq)
+    C = heads * d
+    n = 3
+    nkv = 2 if cross else n
+    q = _vals(rng, (n, nq, C), dt, scale)
+    k = _vals(rng, (nkv, nk, C), dt, scale)
+    v = _vals(rng, (nkv, nk, C), dt)
+    idx = np.array([1, 0, 1], np.int32) if cross else None
+    o = torch.empty(n, nq, C, device="cuda", dtype=_tdt(dt))
+    ops.attention(_dev(q, dt), _dev(k, dt), _dev(v, dt), o, n, heads, d, nq, nk, C, C, C, nq * C, nk * C,
+                  nq * C, 1.0 / math.sqrt(d), kv_index=_dev(idx) if cross else None)
+    torch.cuda.synchronize()
+    got = o.float().cpu().numpy()
+    for i in range(n):
+        j = idx[i] if cross else i
+        ref = O.attention(q[i].astype(np.float64), k[j].astype(np.float64), v[j].astype(np.float64), heads)
+        err = rel_l2(got[i], ref)
+        # fp32 scores carry a relative rounding error ~2^-24 |s|; with logits
+        # scaled x30 (|s| ~ 1e3) that reaches the output as ~1e-4.
+        tol = TOL[dt] if (dt == "bf16" or scale == 1.0) else 2e-4
+        assert err <= tol, (i, err)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("n,H,W,c0,c1,G,eps", [(2, 8, 8, 64, 0, 32, 1e-5), (2, 16, 12, 320, 0, 32, 1e-6),
+                                               (3, 8, 8, 64, 32, 32, 1e-5), (2, 4, 4, 1280, 640, 32, 1e-5),
+                                               (2, 64, 64, 320, 0, 32, 1e-5), (1, 16, 16, 32, 32, 8, 1e-5)])
+def test_groupnorm(ops, dt, n, H, W, c0, c1, G, eps):
+    log(f"groupnorm {dt} {(n, H, W, c0, c1, G)}")
+    rng = np.random.default_rng(c0 + c1 + H)
+    x0 = _vals(rng, (n, H, W, c0), dt, 2.0) + np.float32(0.5)
+    x0 = bf16_round(x0) if dt == "bf16" else x0
+    x1 = _vals(rng, (n, H, W, c1), dt) if c1 else None
+    g = (1 + 0.1 * rng.standard_normal(c0 + c1)).astype(np.float32)
+    b = (0.1 * rng.standard_normal(c0 + c1)).astype(np.float32)
+    sc, sh = ops.groupnorm_stats(_dev(x0, dt), G, eps, _dev(g), _dev(b), x1=_dev(x1, dt) if c1 else None)
+    torch.cuda.synchronize()
+    sc, sh = sc.cpu().numpy().astype(np.float64), sh.cpu().numpy().astype(np.float64)
+    for i in range(n):
+        a = x0[i].astype(np.float64) if not c1 else np.concatenate([x0[i], x1[i]], axis=2).astype(np.float64)
+        ref = O.group_norm(a, G, g, b, eps)
+        err = rel_l2(a * sc[i] + sh[i], ref)
+        assert err <= 1e-5, (i, err)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("T,C", [(37, 64), (300, 320), (64, 1280), (5, 2048)])
+def test_layernorm(ops, dt, T, C):
+    log(f"layernorm {dt} {(T, C)}")
+    rng = np.random.default_rng(T + C)
+    x = _vals(rng, (T, C), dt, 3.0)
+    g = (1 + 0.1 * rng.standard_normal(C)).astype(np.float32)
+    b = (0.1 * rng.standard_normal(C)).astype(np.float32)
+    y = ops.layernorm(_dev(x, dt), _dev(g), _dev(b))
+    torch.cuda.synchronize()
+    err = rel_l2(y.float().cpu().numpy(), O.layer_norm(x.astype(np.float64), g, b))
+    assert err <= (2e-6 if dt == "f32" else 6e-3), err
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_geglu(ops, dt):
+    log(f"geglu {dt}")
+    rng = np.random.default_rng(5)
+    x = _vals(rng, (77, 2 * 320), dt, 2.0)
+    y = ops.geglu(_dev(x, dt))
+    torch.cuda.synchronize()
+    xd = x.astype(np.float64)
+    ref = xd[:, :320] * O.gelu(xd[:, 320:])
+    err = rel_l2(y.float().cpu().numpy(), ref)
+    assert err <= (2e-6 if dt == "f32" else 6e-3), err
