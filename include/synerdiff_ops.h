@@ -30,7 +30,8 @@ extern "C" {
  * when upsampling.  w is the packed weight [cout, ks*ks*cin] (tap-major,
  * channel-minor).  bias may be NULL; resid ([n, Ho, Wo, cout], activation
  * dtype) may be NULL or equal to out.  out_f32 = 1 writes fp32 output.
- * Constraints: ks in {1, 3}; stride in {1, 2}; c0, c1 multiples of 8. */
+ * Constraints: ks in {1, 3}; stride in {1, 2}; c0, c1 multiples of 8;
+ * bf16: cout a multiple of 4. */
 sd_status synerdiff_op_conv(int32_t dtype, const void* d_x0, int32_t c0, const void* d_x1, int32_t c1,
                             int32_t n, int32_t H, int32_t W, int32_t ks, int32_t stride, int32_t up,
                             const float* d_scale, const float* d_shift, int32_t silu, const void* d_w,

@@ -40,6 +40,8 @@ struct Epi {
   void* out;              // [M, ldo]
   int ldo;
   int out_f32;            // 1: fp32 output regardless of the activation dtype
+  int geglu;              // bf16 only: columns packed as 32-blocks [a(16) | gate(16)];
+                          // out[m, 16t + u] = (a + b) * GELU(gate + b), ldo = N / 2
 };
 
 struct GemmArgs {
@@ -50,6 +52,7 @@ struct GemmArgs {
   Epi epi;
 };
 
+// bf16 requires N % 4 == 0, 8-byte aligned outputs and ldo, ldr % 4 == 0.
 hipError_t launch_gemm(DType dt, const GemmArgs& a, hipStream_t s);
 
 // Attention: O = softmax(Q K^T * scale) V per (img, head).
@@ -70,6 +73,10 @@ hipError_t launch_groupnorm_stats(DType dt, const void* src0, int c0, const void
                                   const float* beta, float* partial, float* scale, float* shift,
                                   hipStream_t s);
 size_t groupnorm_partial_floats(int imgs, int hw, int cin);
+// out = act(x * scale + shift) over the concat [src0 | src1] (act = SiLU or identity).
+hipError_t launch_groupnorm_apply(DType dt, const void* src0, int c0, const void* src1, int c1, int imgs,
+                                  int hw, const float* scale, const float* shift, int silu, void* out,
+                                  hipStream_t s);
 
 hipError_t launch_layernorm(DType dt, const void* x, void* y, long tokens, int C, const float* gamma,
                             const float* beta, float eps, hipStream_t s);

@@ -264,6 +264,48 @@ hipError_t launch_groupnorm_stats(DType dt, const void* src0, int c0, const void
   return hipGetLastError();
 }
 
+// Pass 3: y = act(x * scale + shift) into a materialised [imgs, hw, cin]
+// tensor (the concat of the two sources when there are two); one 8-channel
+// vector per thread.
+template <typename T>
+__global__ void gn_apply_kernel(const T* src0, int c0, const T* src1, int c1, const float* scale,
+                                const float* shift, T* out, long n_vec, int hw, int silu) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_vec) return;
+  const int cin = c0 + c1, CV = cin / 8;
+  const long pix = i / CV;
+  const int c = (int)(i - pix * CV) * 8;
+  const int img = (int)(pix / hw);
+  float v[8], sc[8], sh[8];
+  if (c < c0)
+    load8f(src0 + pix * c0 + c, v);
+  else
+    load8f(src1 + pix * c1 + (c - c0), v);
+  load8f(scale + (long)img * cin + c, sc);
+  load8f(shift + (long)img * cin + c, sh);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    v[k] = v[k] * sc[k] + sh[k];
+    if (silu) v[k] = silu_f(v[k]);
+  }
+  store8f(out + pix * cin + c, v);
+}
+
+hipError_t launch_groupnorm_apply(DType dt, const void* src0, int c0, const void* src1, int c1, int imgs,
+                                  int hw, const float* scale, const float* shift, int silu, void* out,
+                                  hipStream_t s) {
+  const long n = (long)imgs * hw * ((c0 + c1) / 8);
+  if (n == 0) return hipSuccess;
+  const unsigned blocks = (unsigned)((n + 255) / 256);
+  if (dt == BF16)
+    gn_apply_kernel<bf16><<<blocks, 256, 0, s>>>((const bf16*)src0, c0, (const bf16*)src1, c1, scale, shift,
+                                                 (bf16*)out, n, hw, silu);
+  else
+    gn_apply_kernel<float><<<blocks, 256, 0, s>>>((const float*)src0, c0, (const float*)src1, c1, scale,
+                                                  shift, (float*)out, n, hw, silu);
+  return hipGetLastError();
+}
+
 // -------------------------------------------------------------- LayerNorm
 // One wave per token; the token's C values stay in registers (C <= 2048).
 template <typename T>

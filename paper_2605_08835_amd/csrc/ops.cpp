@@ -36,6 +36,7 @@ sd_status synerdiff_op_conv(int32_t dtype, const void* x0, int32_t c0, const voi
   if ((ks != 1 && ks != 3) || (stride != 1 && stride != 2) || (up && stride != 1) || (ks == 1 && (stride != 1 || up)))
     return op_fail(SD_ERR_UNSUPPORTED, "unsupported ks/stride/up");
   if (stride == 2 && (H % 2 || W % 2)) return op_fail(SD_ERR_UNSUPPORTED, "stride 2 needs even H, W");
+  if (dtype == SD_BF16 && cout % 4) return op_fail(SD_ERR_UNSUPPORTED, "bf16 needs cout % 4 == 0");
   if (n == 0) return SD_OK;
   GemmArgs a;
   memset(&a, 0, sizeof(a));

@@ -37,7 +37,10 @@ static inline uint16_t f2bf(float f) {
 static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // ------------------------------------------------------------------ layout
-enum PackKind { P_ACT, P_F32, P_F32_SUM, P_CONV3, P_CONV3_SKIP };
+// P_*_GEGLU: rows of the GEGLU projection [a (4C) ; gate (4C)] reordered in
+// blocks of 32 as [a 16t..16t+15 | gate 16t..16t+15] so that one 32-column
+// MFMA tile holds matching value / gate columns.
+enum PackKind { P_ACT, P_F32, P_F32_SUM, P_CONV3, P_CONV3_SKIP, P_ACT_GEGLU, P_F32_GEGLU };
 struct PackJob {
   PackKind kind;
   size_t dst;
@@ -74,7 +77,7 @@ struct LevelW {
 // Workspace roles (buffers sized by a dry run at max capacity).
 enum Role {
   R_X0, R_HA, R_HB, R_U, R_TZ, R_TX, R_TQ, R_TF, R_CTX, R_CKV, R_GNP, R_GNS, R_GNH,
-  R_E, R_A, R_H1, R_TAU, R_T2, R_TB, R_EPS, R_SCAL, R_SKIP0
+  R_E, R_A, R_H1, R_TAU, R_T2, R_TB, R_EPS, R_SCAL, R_GNA, R_SKIP0
 };
 
 }  // namespace sd
@@ -209,8 +212,15 @@ static TxW transformer(sd_unet* h, const std::string& p, int C, int depth) {
     w.o2b = job_f32(h, {b + ".attn2.o.b"}, C);
     w.ln3g = job_f32(h, {b + ".ln3.g"}, C);
     w.ln3b = job_f32(h, {b + ".ln3.b"}, C);
-    w.f1w = job_act(h, {b + ".ff.w1"}, 8 * CC);
-    w.f1b = job_f32(h, {b + ".ff.b1"}, 8 * C);
+    if (h->dt == BF16) {
+      w.f1w = walloc(h, 8 * CC * h->esz);
+      h->jobs.push_back(PackJob{P_ACT_GEGLU, w.f1w, {b + ".ff.w1"}, 0});
+      w.f1b = walloc(h, 8 * (size_t)C * 4);
+      h->jobs.push_back(PackJob{P_F32_GEGLU, w.f1b, {b + ".ff.b1"}, 0});
+    } else {
+      w.f1w = job_act(h, {b + ".ff.w1"}, 8 * CC);
+      w.f1b = job_f32(h, {b + ".ff.b1"}, 8 * C);
+    }
     w.f2w = job_act(h, {b + ".ff.w2"}, 4 * CC);
     w.f2b = job_f32(h, {b + ".ff.b2"}, C);
     t.blk.push_back(w);
@@ -370,6 +380,18 @@ struct Step {
        "groupnorm", K_GN, 3.0 * rows * hw * cin, (double)rows * hw * cin * h->esz + 8.0 * rows * cin);
   }
 
+  // GroupNorm (+ SiLU) of [src0 | src1] materialised as one [rows, hw, cin] tensor.
+  void* gn_norm(const void* s0, int c0, const void* s1, int c1, int hw, float eps, size_t g, size_t b, int silu) {
+    float *sc, *sh;
+    gn(s0, c0, s1, c1, hw, eps, g, b, &sc, &sh);
+    const int cin = c0 + c1;
+    void* out = buf(R_GNA, (size_t)rows * hw * cin * h->esz);
+    if (dry || err) return out;
+    ok(launch_groupnorm_apply(h->dt, s0, c0, s1, c1, rows, hw, sc, sh, silu, out, s), "groupnorm apply", K_GN,
+       (silu ? 6.0 : 2.0) * rows * hw * cin, 2.0 * rows * hw * cin * h->esz);
+    return out;
+  }
+
   static ASeg seg(const void* s0, int c0, const void* s1, int c1, int ks, int stride, int up, int Hi,
                   int Wi, const float* sc, const float* sh, int silu) {
     ASeg a;
@@ -430,18 +452,17 @@ struct Step {
   // ResBlock on [src0 | src1] (H x W) -> out (cout channels).
   void resblock(const ResW& r, const void* s0, int c0, const void* s1, int c1, int H, int W_, void* out,
                 const float* tb) {
-    const int hw = H * W_;
-    float *sc, *sh;
-    gn(s0, c0, s1, c1, hw, 1e-5f, r.n1g, r.n1b, &sc, &sh);
+    const int hw = H * W_, cin = c0 + c1;
+    void* n1 = gn_norm(s0, c0, s1, c1, hw, 1e-5f, r.n1g, r.n1b, 1);
     void* u = buf(R_U, (size_t)rows * hw * r.cout * h->esz);
     Epi e1 = epi(u, r.cout, Wf(r.c1.b));
     e1.tbias = tb;
     e1.tb_ld = h->tb_total;
     e1.tb_off = r.tb_off;
     e1.hw = hw;
-    gemm(seg(s0, c0, s1, c1, 3, 1, 0, H, W_, sc, sh, 1), nullptr, W(r.c1.w), r.cout, e1, "conv1");
-    gn(u, r.cout, nullptr, 0, hw, 1e-5f, r.n2g, r.n2b, &sc, &sh);
-    const ASeg a2 = seg(u, r.cout, nullptr, 0, 3, 1, 0, H, W_, sc, sh, 1);
+    gemm(seg(n1, cin, nullptr, 0, 3, 1, 0, H, W_, nullptr, nullptr, 0), nullptr, W(r.c1.w), r.cout, e1, "conv1");
+    void* n2 = gn_norm(u, r.cout, nullptr, 0, hw, 1e-5f, r.n2g, r.n2b, 1);
+    const ASeg a2 = seg(n2, r.cout, nullptr, 0, 3, 1, 0, H, W_, nullptr, nullptr, 0);
     if (r.skip) {
       const ASeg sk = seg(s0, c0, s1, c1, 1, 1, 0, H, W_, nullptr, nullptr, 0);
       gemm(a2, &sk, W(r.c2.w), r.cout, epi(out, r.cout, Wf(r.c2.b)), "conv2+skip");
@@ -455,15 +476,13 @@ struct Step {
     const int hw = H * W_, C = t.C;
     const long T = (long)rows * hw;
     const int L = h->cfg.ctx_len, D = h->cfg.ctx_dim;
-    float *sc, *sh;
-    gn(hbuf, C, nullptr, 0, hw, 1e-6f, t.ng, t.nb, &sc, &sh);
+    void* nh = gn_norm(hbuf, C, nullptr, 0, hw, 1e-6f, t.ng, t.nb, 0);
     void* z = buf(R_TZ, (size_t)T * C * h->esz);
     void* x = buf(R_TX, (size_t)T * C * h->esz);
     void* q = buf(R_TQ, (size_t)T * 4 * C * h->esz);
-    void* f = buf(R_TF, (size_t)T * 8 * C * h->esz);
+    void* f = h->dt == BF16 ? nullptr : buf(R_TF, (size_t)T * 8 * C * h->esz);
     void* ckv = buf(R_CKV, (size_t)(n_req + 1) * L * 2 * C * h->esz);
-    gemm(seg(hbuf, C, nullptr, 0, 1, 1, 0, H, W_, sc, sh, 0), nullptr, W(t.piw), C, epi(z, C, Wf(t.pib)),
-         "proj_in");
+    gemm(lin(nh, C, T), nullptr, W(t.piw), C, epi(z, C, Wf(t.pib)), "proj_in", T);
     for (const BlkW& b : t.blk) {
       if (!dry && !err) ok(launch_layernorm(h->dt, z, x, T, C, Wf(b.ln1g), Wf(b.ln1b), 1e-5f, s), "ln1", K_LN, 8.0 * T * C, 2.0 * T * C * h->esz);
       gemm(lin(x, C, T), nullptr, W(b.qkv), 3 * C, epi(q, 3 * C, nullptr), "qkv", T);
@@ -496,8 +515,15 @@ struct Step {
       }
       gemm(lin(x, C, T), nullptr, W(b.o2w), C, epi(z, C, Wf(b.o2b), z, C), "attn2.out", T);
       if (!dry && !err) ok(launch_layernorm(h->dt, z, x, T, C, Wf(b.ln3g), Wf(b.ln3b), 1e-5f, s), "ln3", K_LN, 8.0 * T * C, 2.0 * T * C * h->esz);
-      gemm(lin(x, C, T), nullptr, W(b.f1w), 8 * C, epi(f, 8 * C, Wf(b.f1b)), "ff1", T);
-      if (!dry && !err) ok(launch_geglu(h->dt, f, q, T, 4 * C, s), "geglu", K_GEGLU, 4.0 * T * 4 * C, 12.0 * T * C * h->esz);
+      if (h->dt == BF16) {  // GEGLU fused into the projection's epilogue
+        Epi ef = epi(q, 4 * C, Wf(b.f1b));
+        ef.geglu = 1;
+        gemm(lin(x, C, T), nullptr, W(b.f1w), 8 * C, ef, "ff1+geglu", T);
+      } else {
+        gemm(lin(x, C, T), nullptr, W(b.f1w), 8 * C, epi(f, 8 * C, Wf(b.f1b)), "ff1", T);
+        if (!dry && !err)
+          ok(launch_geglu(h->dt, f, q, T, 4 * C, s), "geglu", K_GEGLU, 4.0 * T * 4 * C, 12.0 * T * C * h->esz);
+      }
       gemm(lin(q, 4 * C, T), nullptr, W(b.f2w), C, epi(z, C, Wf(b.f2b), z, C), "ff2", T);
     }
     gemm(lin(z, C, T), nullptr, W(t.pow), C, epi(hbuf, C, Wf(t.pob), hbuf, C), "proj_out", T);
@@ -623,12 +649,12 @@ struct Step {
       }
     }
     // output: GN + SiLU + conv (fp32 eps rows), then CFG combine + DDIM
-    float *sc, *sh;
-    gn(cur, curc, nullptr, 0, H * Wd, 1e-5f, h->outg, h->outb, &sc, &sh);
+    void* no = gn_norm(cur, curc, nullptr, 0, H * Wd, 1e-5f, h->outg, h->outb, 1);
     float* eps = (float*)buf(R_EPS, (size_t)rows * H * Wd * c.latent_c * 4);
     Epi eo = epi(eps, c.latent_c, Wf(h->conv_out.b));
     eo.out_f32 = 1;
-    gemm(seg(cur, curc, nullptr, 0, 3, 1, 0, H, Wd, sc, sh, 1), nullptr, W(h->conv_out.w), c.latent_c, eo, "conv_out");
+    gemm(seg(no, curc, nullptr, 0, 3, 1, 0, H, Wd, nullptr, nullptr, 0), nullptr, W(h->conv_out.w), c.latent_c, eo,
+         "conv_out");
     if (!dry && !err)
       ok(launch_cfg_ddim(eps, lat_in, lat_out, eps_out, n_req, c.latent_c, H * Wd, req_row_u, req_coef, s),
          "cfg+ddim", K_CFG, 4.0 * n_req * c.latent_c * H * Wd,
@@ -819,6 +845,23 @@ sd_status synerdiff_load_weights(sd_unet* h, const float* hp, size_t n_floats, v
         for (auto* p : src) {
           memcpy(&host[j.dst + o * 4], hp + p->offset, p->numel * 4);
           o += p->numel;
+        }
+        break;
+      }
+      case P_ACT_GEGLU:
+      case P_F32_GEGLU: {
+        const Param* p = src[0];
+        const size_t rows8 = (size_t)p->shape[0], half = rows8 / 2, cols = p->numel / rows8;
+        for (size_t r = 0; r < rows8; ++r) {
+          const size_t t = r / 32, u = r % 32;
+          const size_t srow = u < 16 ? 16 * t + u : half + 16 * t + (u - 16);
+          for (size_t k = 0; k < cols; ++k) {
+            const float v = hp[p->offset + srow * cols + k];
+            if (j.kind == P_ACT_GEGLU)
+              put_act(j.dst, r * cols + k, v);
+            else
+              memcpy(&host[j.dst + (r * cols + k) * 4], &v, 4);
+          }
         }
         break;
       }
