@@ -142,10 +142,6 @@ __device__ inline void epilogue4(const Epi& e, int m, int n, float x[4]) {
 // padded by 16 bytes so the 16-byte fragment reads of 8 consecutive rows hit
 // distinct banks.  Blocks are renumbered so that the tiles sharing one A
 // row band run on the same XCD (blocks are dealt round-robin over 8 XCDs).
-namespace mf {
-constexpr int BK = 64, LDS_LD = BK + 8;
-}
-
 template <int V>
 struct IC {
   static constexpr int value = V;
@@ -158,16 +154,34 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
-// FAST: every segment is a stride-1 3x3 or 1x1 layer on an image of the
-// output's size, with cin and the source split c0 multiples of BK, so each
-// K tile lies in one (segment, tap, source) and the input pixel of row m
-// under tap (ky, kx) is m + (ky-1) W + (kx-1): the per-tile addressing is
-// uniform and each row keeps only m and a 9-bit mask of in-image taps.
-template <int BM, int BN, int WM, int WN, bool AFF, bool FAST>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) void gemm_bf16_kernel(GemmArgs a) {
-  using namespace mf;
+// Loader modes.
+//  0: per-thread addressing of any layer (incl. the GroupNorm affine on load).
+//  1: every segment is a stride-1 3x3 or 1x1 layer on an image of the
+//     output's size with cin and the source split c0 multiples of BK, so a
+//     K tile lies in one (segment, tap, source) and the input pixel of row m
+//     under tap (ky, kx) is m + (ky-1) W + (kx-1): the tile's addressing is
+//     uniform and each row keeps only m and a 9-bit mask of in-image taps.
+//  2: one stride-2 or upsampling 3x3 segment with cin a multiple of BK:
+//     uniform tap per tile, rows keep (image base pixel, oy, ox).
+// Modes 1 and 2 read through buffer resources: a masked-off element gets an
+// out-of-range offset, which the hardware returns as zero, so the loads are
+// branch-free.
+constexpr int OOB = (int)0x80000000u;
+
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, long bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ inline bf16x8 buf_load16(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int MODE, int MINB>
+__global__ __launch_bounds__(256, MINB) void gemm_bf16_kernel(GemmArgs a) {
+  constexpr int LDS_LD = BK + 8;
   constexpr int TM = BM / WM / 32, TN = BN / WN / 32;  // 32x32 tiles per wave
-  constexpr int AR = BM / 32, BR = BN / 32;             // 16-byte chunks per thread
+  constexpr int CPR = BK / 8, RPP = 256 / CPR;         // chunks per row, rows per pass
+  constexpr int AR = (BM + RPP - 1) / RPP, BR = (BN + RPP - 1) / RPP;  // 16-byte chunks per thread
+  static_assert(BM % RPP == 0, "A tile rows must be a multiple of the rows per loader pass");
   __shared__ __attribute__((aligned(16))) bf16 As[2][BM * LDS_LD];
   __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN * LDS_LD];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -179,68 +193,112 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
   const int tm = bid / tiles_n, tn = bid - tm * tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
 
-  const int kc = tid & 7, lrow = tid >> 3;  // loader: chunk kc of rows lrow + 32 j
-  RowPos rp[FAST ? 1 : AR];
-  int fm[FAST ? AR : 1], fmask[FAST ? AR : 1];
-  if constexpr (FAST) {
-    const int W = a.seg[0].Wo, H = a.seg[0].Ho, hw = H * W;
+  const int kc = tid % CPR, lrow = tid / CPR;  // loader: chunk kc of rows lrow + RPP j
+  constexpr int NR = MODE == 0 ? 1 : AR;
+  RowPos rp[MODE == 0 ? AR : 1];
+  int ra0[NR], ra1[NR];  // mode 1: (m, tap mask); mode 2: (image base pixel, oy << 16 | ox)
+  const int Ho = a.seg[0].Ho, Wo = a.seg[0].Wo, hwo = Ho * Wo;
+  if constexpr (MODE == 1) {
 #pragma unroll
     for (int j = 0; j < AR; ++j) {
-      const int m = m0 + lrow + 32 * j;
-      const int p = m % hw, oy = p / W, ox = p - oy * W;
+      const int m = m0 + lrow + RPP * j;
+      const int p = m % hwo, oy = p / Wo, ox = p - oy * Wo;
       int mk = 0;
 #pragma unroll
       for (int t = 0; t < 9; ++t) {
         const int iy = oy + t / 3 - 1, ix = ox + t % 3 - 1;
-        if (iy >= 0 && iy < H && ix >= 0 && ix < W) mk |= 1 << t;
+        if (iy >= 0 && iy < Ho && ix >= 0 && ix < Wo) mk |= 1 << t;
       }
-      fm[j] = m;
-      fmask[j] = m < a.M ? mk : 0;
+      ra0[j] = m;
+      ra1[j] = m < a.M ? mk : 0;
+    }
+  } else if constexpr (MODE == 2) {
+#pragma unroll
+    for (int j = 0; j < AR; ++j) {
+      const int m = m0 + lrow + RPP * j;
+      const int img = m / hwo, p = m - img * hwo, oy = p / Wo, ox = p - oy * Wo;
+      ra0[j] = img * a.seg[0].Hi * a.seg[0].Wi;
+      ra1[j] = m < a.M ? (oy << 16) | ox : -1;
     }
   } else {
 #pragma unroll
-    for (int j = 0; j < AR; ++j) rp[j] = decode_row(a.seg[0], m0 + lrow + 32 * j, a.M);
+    for (int j = 0; j < AR; ++j) rp[j] = decode_row(a.seg[0], m0 + lrow + RPP * j, a.M);
   }
-  const bf16* B = reinterpret_cast<const bf16*>(a.B);
+  const __amdgpu_buffer_rsrc_t bres = make_rsrc(a.B, (long)a.N * a.ldb * 2);
+  int boff[BR];
+#pragma unroll
+  for (int j = 0; j < BR; ++j) {
+    const int n = n0 + lrow + RPP * j;
+    boff[j] = (n < a.N && lrow + RPP * j < BN) ? n * a.ldb * 2 : OOB;
+  }
 
   bf16x8 ra[AR], rb[BR];
+  // Uniform loader state of the next K tile (modes 1, 2): segment, tap and
+  // channel base, advanced by BK per tile without divisions.
+  int st_seg = 0, st_tap = 0, st_cb = 0;
   auto gload = [&](int kt) {
     const int k = kt * BK + kc * 8;
     const bf16x8 z = {};
-    if constexpr (FAST) {
-      // uniform per tile: segment, tap, source and channel base
+    if constexpr (MODE != 0) {
+      // (fields are picked one by one: selecting a whole kernel-argument
+      // struct by a runtime condition would copy it to scratch)
       const int k0 = kt * BK;
-      // (fields picked one by one: selecting a whole kernel-argument struct
-      // by a runtime condition would copy it to scratch)
-      const bool s1 = k0 >= a.seg[0].K;
-      const int kk = s1 ? k0 - a.seg[0].K : k0;
+      const bool s1 = MODE == 1 && st_seg;
       const int gcin = s1 ? a.seg[1].cin : a.seg[0].cin, gks = s1 ? a.seg[1].ks : a.seg[0].ks;
       const int gc0 = s1 ? a.seg[1].c0 : a.seg[0].c0, gc1 = s1 ? a.seg[1].c1 : a.seg[0].c1;
       const void* gs0 = s1 ? a.seg[1].src0 : a.seg[0].src0;
       const void* gs1 = s1 ? a.seg[1].src1 : a.seg[0].src1;
-      const int tap = kk / gcin, cb = kk - tap * gcin;
-      const int t9 = gks == 3 ? tap : 4;  // a 1x1 tap is the centre of the 3x3 mask
-      const int dpix = gks == 3 ? (tap / 3 - 1) * a.seg[0].Wo + (tap % 3 - 1) : 0;
+      const int tap = st_tap, cb = st_cb;
+      st_cb += BK;
+      if (st_cb >= gcin) {
+        st_cb = 0;
+        if (++st_tap == gks * gks) {
+          st_tap = 0;
+          st_seg = 1;
+        }
+      }
       const bool in0 = cb < gc0;
-      const bf16* src = reinterpret_cast<const bf16*>(in0 ? gs0 : gs1);
-      const int cs = in0 ? gc0 : gc1, c = (in0 ? cb : cb - gc0) + kc * 8;
+      const int cs = in0 ? gc0 : gc1, c2 = 2 * ((in0 ? cb : cb - gc0) + kc * 8);
       const bool live = k0 < a.K;
+      if constexpr (MODE == 1) {
+        const long npix = a.M;
+        const __amdgpu_buffer_rsrc_t ares = make_rsrc(in0 ? gs0 : gs1, npix * cs * 2);
+        const int t9 = gks == 3 ? tap : 4;  // a 1x1 tap is the centre of the 3x3 mask
+        const int dpix = gks == 3 ? (tap / 3 - 1) * Wo + (tap % 3 - 1) : 0;
 #pragma unroll
-      for (int j = 0; j < AR; ++j) {
-        const bool ok = live && ((fmask[j] >> t9) & 1);
-        ra[j] = ok ? *reinterpret_cast<const bf16x8*>(src + (long)(fm[j] + dpix) * cs + c) : z;
+        for (int j = 0; j < AR; ++j) {
+          const bool ok = live && ((ra1[j] >> t9) & 1);
+          ra[j] = buf_load16(ares, ok ? (ra0[j] + dpix) * cs * 2 + c2 : OOB);
+        }
+      } else {
+        const ASeg& g = a.seg[0];
+        const long npix = (long)(a.M / hwo) * g.Hi * g.Wi;
+        const __amdgpu_buffer_rsrc_t ares = make_rsrc(in0 ? gs0 : gs1, npix * cs * 2);
+        const int ky = tap / 3 - 1, kx = tap % 3 - 1;
+#pragma unroll
+        for (int j = 0; j < AR; ++j) {
+          const int oy = ra1[j] >> 16, ox = ra1[j] & 0xFFFF;
+          int iy, ix;
+          bool ok;
+          if (g.up) {
+            iy = oy + ky;
+            ix = ox + kx;
+            ok = iy >= 0 && iy < 2 * g.Hi && ix >= 0 && ix < 2 * g.Wi;
+            iy >>= 1;
+            ix >>= 1;
+          } else {
+            iy = oy * g.stride + ky;
+            ix = ox * g.stride + kx;
+            ok = iy >= 0 && iy < g.Hi && ix >= 0 && ix < g.Wi;
+          }
+          ok = ok && live && ra1[j] >= 0;
+          ra[j] = buf_load16(ares, ok ? (ra0[j] + iy * g.Wi + ix) * cs * 2 + c2 : OOB);
+        }
       }
     } else if (k < a.seg[0].K) {
       const int tap = k / a.seg[0].cin, c = k - tap * a.seg[0].cin;
 #pragma unroll
-      for (int j = 0; j < AR; ++j) {
-        if (AFF) {
-          ra[j] = a_chunk_bf16(a.seg[0], rp[j], tap, c);
-        } else {
-          const bf16* p = a_chunk_ptr<bf16>(a.seg[0], rp[j], tap, c);
-          ra[j] = p ? *reinterpret_cast<const bf16x8*>(p) : z;
-        }
-      }
+      for (int j = 0; j < AR; ++j) ra[j] = a_chunk_bf16(a.seg[0], rp[j], tap, c);
     } else if (k < a.K) {
       const int kk = k - a.seg[0].K;
       const int tap = kk / a.seg[1].cin, c = kk - tap * a.seg[1].cin;
@@ -253,17 +311,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
 #pragma unroll
       for (int j = 0; j < AR; ++j) ra[j] = z;
     }
+    const bool kin = k < a.K;
 #pragma unroll
-    for (int j = 0; j < BR; ++j) {
-      const int n = n0 + lrow + 32 * j;
-      rb[j] = (n < a.N && k < a.K) ? *reinterpret_cast<const bf16x8*>(B + (long)n * a.ldb + k) : z;
-    }
+    for (int j = 0; j < BR; ++j) rb[j] = buf_load16(bres, kin ? boff[j] + 2 * k : OOB);
   };
   auto sstore = [&](int buf) {
 #pragma unroll
-    for (int j = 0; j < AR; ++j) *reinterpret_cast<bf16x8*>(&As[buf][(lrow + 32 * j) * LDS_LD + kc * 8]) = ra[j];
+    for (int j = 0; j < AR; ++j) *reinterpret_cast<bf16x8*>(&As[buf][(lrow + RPP * j) * LDS_LD + kc * 8]) = ra[j];
 #pragma unroll
-    for (int j = 0; j < BR; ++j) *reinterpret_cast<bf16x8*>(&Bs[buf][(lrow + 32 * j) * LDS_LD + kc * 8]) = rb[j];
+    for (int j = 0; j < BR; ++j)
+      if (BN % RPP == 0 || lrow + RPP * j < BN)
+        *reinterpret_cast<bf16x8*>(&Bs[buf][(lrow + RPP * j) * LDS_LD + kc * 8]) = rb[j];
   };
 
   f32x16 acc[TM][TN];
@@ -422,54 +480,77 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
     }
 }
 
-static bool fast_seg(const ASeg& g, int Ho, int Wo) {
+static bool fast_seg(const ASeg& g, int Ho, int Wo, int BK) {
   return g.stride == 1 && !g.up && (g.ks == 1 || g.ks == 3) && g.Hi == Ho && g.Wi == Wo &&
-         g.cin % mf::BK == 0 && (g.c1 == 0 || g.c0 % mf::BK == 0) && g.scale == nullptr;
+         g.cin % BK == 0 && (g.c1 == 0 || g.c0 % BK == 0) && g.scale == nullptr;
 }
 
-template <int BM, int BN, int WM, int WN>
+// Loader mode of a GEMM (see the kernel); modes 1 and 2 address each source
+// with 32-bit byte offsets, so its bytes must stay below 2^31.
+static int loader_mode(const GemmArgs& a, int BK) {
+  const ASeg& g0 = a.seg[0];
+  const long hwo = (long)g0.Ho * g0.Wo;
+  if (hwo <= 0 || g0.scale) return 0;
+  auto small = [&](const ASeg& g, long npix) {
+    return npix * (long)g.c0 * 2 < (1L << 31) && npix * (long)g.c1 * 2 < (1L << 31);
+  };
+  if (fast_seg(g0, g0.Ho, g0.Wo, BK) && (a.seg[1].K == 0 || fast_seg(a.seg[1], g0.Ho, g0.Wo, BK)) && small(g0, a.M) &&
+      (a.seg[1].K == 0 || small(a.seg[1], a.M)) && (long)a.N * a.ldb * 2 < (1L << 31))
+    return 1;
+  if (a.seg[1].K == 0 && g0.ks == 3 && (g0.stride == 2 || g0.up) && g0.c1 == 0 && g0.cin % BK == 0 &&
+      (a.M / hwo) * (long)g0.Hi * g0.Wi * g0.c0 * 2 < (1L << 31) && (long)a.N * a.ldb * 2 < (1L << 31) &&
+      g0.Ho < 65536 && g0.Wo < 65536)
+    return 2;
+  return 0;
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int MINB = 1>
 static void launch_bf16(const GemmArgs& a, hipStream_t s) {
   const long blocks = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  const ASeg& g0 = a.seg[0];
-  const bool fast = fast_seg(g0, g0.Ho, g0.Wo) && (a.seg[1].K == 0 || fast_seg(a.seg[1], g0.Ho, g0.Wo)) &&
-                    g0.Ho * g0.Wo > 0;
-  if (fast)
-    gemm_bf16_kernel<BM, BN, WM, WN, false, true><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(a);
-  else if (g0.scale)
-    gemm_bf16_kernel<BM, BN, WM, WN, true, false><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(a);
-  else
-    gemm_bf16_kernel<BM, BN, WM, WN, false, false><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(a);
+  const dim3 g((unsigned)blocks), b(256);
+  switch (loader_mode(a, BK)) {
+    case 1: gemm_bf16_kernel<BM, BN, BK, WM, WN, 1, MINB><<<g, b, 0, s>>>(a); break;
+    case 2: gemm_bf16_kernel<BM, BN, BK, WM, WN, 2, MINB><<<g, b, 0, s>>>(a); break;
+    default: gemm_bf16_kernel<BM, BN, BK, WM, WN, 0, MINB><<<g, b, 0, s>>>(a); break;
+  }
 }
 
-// Tile choice: the widest N tile that divides N (160 covers every SD-1.5 /
-// SDXL width: 320, 640, 1280 and their 2x, 3x, 4x, 8x), then the tallest M
-// tile that still gives every CU about two blocks.  The choice depends on
-// the layer shape and the row count only through M, and no K is split, so a
-// row's result never depends on its batch-mates.
+// Tile choice: the widest N tile that divides N (320 and 160 cover every
+// SD-1.5 / SDXL width: 320, 640, 1280 and their 2x, 3x, 4x, 8x), then the
+// tallest M tile that still gives every CU about two blocks.  The choice
+// depends on the layer shape and the row count only through M, and no K is
+// split, so a row's result never depends on its batch-mates.
 hipError_t launch_gemm(DType dt, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   if (dt == BF16 && (a.N % 4 || a.epi.ldo % 4 || (a.epi.resid && a.epi.ldr % 4) || (a.epi.geglu && a.N % 32)))
     return hipErrorInvalidValue;
   if (dt != BF16 && a.epi.geglu) return hipErrorInvalidValue;
+  if ((long)a.N * a.ldb * (dt == BF16 ? 2 : 4) >= (1L << 31)) return hipErrorInvalidValue;
   if (dt == BF16) {
     auto nblk = [&](int bm, int bn) { return (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn); };
     const long want = 2 * 256;
     if (a.N % 160 == 0) {
-      if (nblk(256, 160) >= want)
-        launch_bf16<256, 160, 4, 1>(a, s);
+      // 256x160 tiles, BK 32, two blocks per CU (acc in VGPRs, 2 waves/SIMD)
+      // when the loader is uniform; otherwise 64-deep tiles, one block per CU.
+      if (nblk(256, 160) >= want && loader_mode(a, 32) != 0)
+        launch_bf16<256, 160, 32, 4, 1, 2>(a, s);
+      else if (nblk(256, 160) >= want)
+        launch_bf16<256, 160, 64, 4, 1>(a, s);
+      else if (loader_mode(a, 32) != 0)
+        launch_bf16<128, 160, 32, 4, 1, 2>(a, s);
       else
-        launch_bf16<128, 160, 4, 1>(a, s);
+        launch_bf16<128, 160, 64, 4, 1>(a, s);
     } else if (a.N % 128 == 0 || a.N > 64) {
       if (nblk(256, 128) >= want)
-        launch_bf16<256, 128, 2, 2>(a, s);
+        launch_bf16<256, 128, 64, 2, 2>(a, s);
       else if (nblk(128, 128) >= want)
-        launch_bf16<128, 128, 2, 2>(a, s);
+        launch_bf16<128, 128, 64, 2, 2>(a, s);
       else
-        launch_bf16<64, 128, 2, 2>(a, s);
+        launch_bf16<64, 128, 64, 2, 2>(a, s);
     } else if (a.N > 32) {
-      launch_bf16<128, 64, 4, 1>(a, s);
+      launch_bf16<128, 64, 64, 4, 1>(a, s);
     } else {
-      launch_bf16<256, 32, 4, 1>(a, s);
+      launch_bf16<256, 32, 64, 4, 1>(a, s);
     }
   } else {
     const long blocks = (long)((a.M + sf::BM - 1) / sf::BM) * ((a.N + sf::BN - 1) / sf::BN);
