@@ -39,13 +39,16 @@ sd_status synerdiff_op_conv(int32_t dtype, const void* d_x0, int32_t c0, const v
                             int32_t out_f32, void* hip_stream);
 
 /* Multi-head attention O = softmax(Q K^T * scale) V per image and head
- * (head h uses columns [h*d, (h+1)*d) of each token's row).  Q: image i,
- * token t at q + i*q_img + t*q_ld; K and V likewise with kv_img, kv_ld and
- * image kv_index[i] (d_kv_index NULL = image i); O like Q with o_img, o_ld.
- * Strides in elements.  Constraints: d a multiple of 8; bf16: d <= 256 and
- * not in (192, 224]; fp32: d <= 64. */
+ * (head h uses channels [h*d, (h+1)*d)).  Q: image i, token t, channel c at
+ * q + i*q_img + t*q_ld + c; K likewise with k_img, k_ld and image
+ * kv_index[i] (d_kv_index NULL = image i); V likewise with v_img, v_ld, or,
+ * when v_transposed = 1 (bf16 only), at v + j*v_img + c*v_ld + t (channel-
+ * major, the layout the step's projections write); O like Q with o_img,
+ * o_ld.  Strides in elements.  Constraints: d a multiple of 8; bf16:
+ * d <= 256 and not in (192, 224]; fp32: d <= 64. */
 sd_status synerdiff_op_attention(int32_t dtype, const void* d_q, int64_t q_ld, int64_t q_img,
-                                 const void* d_k, const void* d_v, int64_t kv_ld, int64_t kv_img,
+                                 const void* d_k, int64_t k_ld, int64_t k_img, const void* d_v,
+                                 int64_t v_ld, int64_t v_img, int32_t v_transposed,
                                  const int32_t* d_kv_index, void* d_o, int64_t o_ld, int64_t o_img,
                                  int32_t n, int32_t heads, int32_t d, int32_t n_q, int32_t n_k,
                                  float scale, void* hip_stream);

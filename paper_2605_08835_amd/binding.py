@@ -62,9 +62,10 @@ _SIG = {
                                               ctypes.POINTER(ctypes.c_int32), ctypes.c_int32]),
     "synerdiff_op_conv": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, _P] + [ctypes.c_int32] * 7 +
                           [_P, _P, ctypes.c_int32, _P, ctypes.c_int32, _P, _P, _P, ctypes.c_int32, _P]),
-    "synerdiff_op_attention": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int64, ctypes.c_int64, _P, _P,
-                                              ctypes.c_int64, ctypes.c_int64, _P, _P, ctypes.c_int64,
-                                              ctypes.c_int64] + [ctypes.c_int32] * 5 + [ctypes.c_float, _P]),
+    "synerdiff_op_attention": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int64, ctypes.c_int64, _P,
+                                              ctypes.c_int64, ctypes.c_int64, _P, ctypes.c_int64, ctypes.c_int64,
+                                              ctypes.c_int32, _P, _P, ctypes.c_int64, ctypes.c_int64] +
+                               [ctypes.c_int32] * 5 + [ctypes.c_float, _P]),
     "synerdiff_op_groupnorm_scratch_floats": (ctypes.c_size_t, [ctypes.c_int32] * 3),
     "synerdiff_op_groupnorm_stats": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, _P] + [ctypes.c_int32] * 4 +
                                      [ctypes.c_float, _P, _P, _P, _P, _P, _P]),

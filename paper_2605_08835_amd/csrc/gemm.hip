@@ -396,7 +396,16 @@ __global__ __launch_bounds__(256, MINB) void gemm_bf16_kernel(GemmArgs a) {
             const int n = nt + 8 * q + hq;
             if (n < a.N) {
               float x[4] = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
-              epilogue4<bf16>(a.epi, m, n, x);
+              if (a.epi.vt_out && n >= a.epi.vt_col0) {
+                // transposed store: lanes l and l+1 hold consecutive tokens
+                const int img = m / a.epi.vt_hw, tok = m - img * a.epi.vt_hw;
+                bf16* o = reinterpret_cast<bf16*>(a.epi.vt_out) + (long)img * a.epi.vt_img +
+                          (long)(n - a.epi.vt_col0) * a.epi.vt_ld + tok;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[(long)e * a.epi.vt_ld] = (bf16)x[e];
+              } else {
+                epilogue4<bf16>(a.epi, m, n, x);
+              }
             }
           }
         }
@@ -524,7 +533,9 @@ hipError_t launch_gemm(DType dt, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   if (dt == BF16 && (a.N % 4 || a.epi.ldo % 4 || (a.epi.resid && a.epi.ldr % 4) || (a.epi.geglu && a.N % 32)))
     return hipErrorInvalidValue;
-  if (dt != BF16 && a.epi.geglu) return hipErrorInvalidValue;
+  if (dt != BF16 && (a.epi.geglu || a.epi.vt_out)) return hipErrorInvalidValue;
+  if (a.epi.vt_out && (a.epi.vt_col0 % 8 || a.epi.resid || a.epi.bias || a.epi.tbias || a.epi.out_f32))
+    return hipErrorInvalidValue;
   if ((long)a.N * a.ldb * (dt == BF16 ? 2 : 4) >= (1L << 31)) return hipErrorInvalidValue;
   if (dt == BF16) {
     auto nblk = [&](int bm, int bn) { return (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn); };

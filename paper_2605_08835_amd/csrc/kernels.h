@@ -42,6 +42,10 @@ struct Epi {
   int out_f32;            // 1: fp32 output regardless of the activation dtype
   int geglu;              // bf16 only: columns packed as 32-blocks [a(16) | gate(16)];
                           // out[m, 16t + u] = (a + b) * GELU(gate + b), ldo = N / 2
+  void* vt_out;           // bf16 only: columns n >= vt_col0 are written transposed,
+  int vt_col0, vt_hw;     //   vt_out[(m / vt_hw) * vt_img + (n - vt_col0) * vt_ld + m % vt_hw]
+  int vt_ld;
+  long vt_img;
 };
 
 struct GemmArgs {
@@ -57,8 +61,10 @@ hipError_t launch_gemm(DType dt, const GemmArgs& a, hipStream_t s);
 
 // Attention: O = softmax(Q K^T * scale) V per (img, head).
 struct AttnArgs {
-  const void* q; long q_ld, q_img;   // token stride, image stride (elements)
-  const void* k; const void* v; long kv_ld, kv_img;
+  const void* q; long q_ld, q_img;   // Q[img][token][c]: token stride, image stride (elements)
+  const void* k; long k_ld, k_img;   // K likewise
+  const void* v; long v_ld, v_img;   // V: vt = 0 like K; vt = 1 transposed, V[img][c][token] at
+  int vt;                            //    v + img*v_img + c*v_ld + token (bf16 only)
   const int* kv_index;               // kv image of each q image, or null (= same)
   void* o; long o_ld, o_img;
   int imgs, heads, d, Nq, Nk;

@@ -77,7 +77,7 @@ struct LevelW {
 // Workspace roles (buffers sized by a dry run at max capacity).
 enum Role {
   R_X0, R_HA, R_HB, R_U, R_TZ, R_TX, R_TQ, R_TF, R_CTX, R_CKV, R_GNP, R_GNS, R_GNH,
-  R_E, R_A, R_H1, R_TAU, R_T2, R_TB, R_EPS, R_SCAL, R_GNA, R_SKIP0
+  R_E, R_A, R_H1, R_TAU, R_T2, R_TB, R_EPS, R_SCAL, R_GNA, R_TV, R_CVT, R_SKIP0
 };
 
 }  // namespace sd
@@ -482,14 +482,35 @@ struct Step {
     void* q = buf(R_TQ, (size_t)T * 4 * C * h->esz);
     void* f = h->dt == BF16 ? nullptr : buf(R_TF, (size_t)T * 8 * C * h->esz);
     void* ckv = buf(R_CKV, (size_t)(n_req + 1) * L * 2 * C * h->esz);
+    const int Lp = (L + 7) / 8 * 8;
+    void* vbuf = h->dt == BF16 ? buf(R_TV, (size_t)T * C * h->esz) : nullptr;
+    void* cvt = h->dt == BF16 ? buf(R_CVT, (size_t)(n_req + 1) * C * Lp * h->esz) : nullptr;
     gemm(lin(nh, C, T), nullptr, W(t.piw), C, epi(z, C, Wf(t.pib)), "proj_in", T);
     for (const BlkW& b : t.blk) {
       if (!dry && !err) ok(launch_layernorm(h->dt, z, x, T, C, Wf(b.ln1g), Wf(b.ln1b), 1e-5f, s), "ln1", K_LN, 8.0 * T * C, 2.0 * T * C * h->esz);
-      gemm(lin(x, C, T), nullptr, W(b.qkv), 3 * C, epi(q, 3 * C, nullptr), "qkv", T);
+      // bf16: Q|K row-major [T, 2C], V transposed per image [rows][C][hw]
+      // (the layout the attention kernel stages with 16-byte loads).
+      const bool vt = h->dt == BF16;
+      Epi eq = epi(q, vt ? 2 * C : 3 * C, nullptr);
+      if (vt) {
+        eq.vt_out = vbuf;
+        eq.vt_col0 = 2 * C;
+        eq.vt_hw = hw;
+        eq.vt_ld = hw;
+        eq.vt_img = (long)C * hw;
+      }
+      gemm(lin(x, C, T), nullptr, W(b.qkv), 3 * C, eq, "qkv", T);
       if (!dry && !err) {
         AttnArgs a;
-        a.q = q; a.q_ld = 3 * C; a.q_img = (long)hw * 3 * C;
-        a.k = at(q, C); a.v = at(q, 2 * C); a.kv_ld = 3 * C; a.kv_img = (long)hw * 3 * C;
+        memset(&a, 0, sizeof(a));
+        const long qld = vt ? 2 * C : 3 * C;
+        a.q = q; a.q_ld = qld; a.q_img = (long)hw * qld;
+        a.k = at(q, C); a.k_ld = qld; a.k_img = (long)hw * qld;
+        if (vt) {
+          a.v = vbuf; a.v_ld = hw; a.v_img = (long)C * hw; a.vt = 1;
+        } else {
+          a.v = at(q, 2 * C); a.v_ld = qld; a.v_img = (long)hw * qld;
+        }
         a.kv_index = nullptr;
         a.o = x; a.o_ld = C; a.o_img = (long)hw * C;
         a.imgs = rows; a.heads = t.heads; a.d = t.d; a.Nq = hw; a.Nk = hw;
@@ -500,18 +521,35 @@ struct Step {
       gemm(lin(x, C, T), nullptr, W(b.o1w), C, epi(z, C, Wf(b.o1b), z, C), "attn1.out", T);
       if (!dry && !err) ok(launch_layernorm(h->dt, z, x, T, C, Wf(b.ln2g), Wf(b.ln2b), 1e-5f, s), "ln2", K_LN, 8.0 * T * C, 2.0 * T * C * h->esz);
       gemm(lin(x, C, T), nullptr, W(b.q2), C, epi(q, C, nullptr), "attn2.q", T);
-      gemm(lin(ctx, D, (long)(n_req + 1) * L), nullptr, W(b.kv2), 2 * C, epi(ckv, 2 * C, nullptr), "attn2.kv",
-           (long)(n_req + 1) * L);
-      if (!dry && !err) {
-        AttnArgs a;
-        a.q = q; a.q_ld = C; a.q_img = (long)hw * C;
-        a.k = ckv; a.v = at(ckv, C); a.kv_ld = 2 * C; a.kv_img = (long)L * 2 * C;
-        a.kv_index = row_ctx;
-        a.o = x; a.o_ld = C; a.o_img = (long)hw * C;
-        a.imgs = rows; a.heads = t.heads; a.d = t.d; a.Nq = hw; a.Nk = L;
-        a.scale = 1.0f / sqrtf((float)t.d);
-        ok(launch_attention(h->dt, a, s), "cross-attention", K_ATTN, 4.0 * rows * hw * (double)L * C,
-           (2.0 * T * C + 2.0 * (n_req + 1) * L * C) * h->esz);
+      {
+        const bool vt = h->dt == BF16;
+        Epi ek = epi(ckv, vt ? C : 2 * C, nullptr);
+        if (vt) {
+          ek.vt_out = cvt;
+          ek.vt_col0 = C;
+          ek.vt_hw = L;
+          ek.vt_ld = Lp;
+          ek.vt_img = (long)C * Lp;
+        }
+        gemm(lin(ctx, D, (long)(n_req + 1) * L), nullptr, W(b.kv2), 2 * C, ek, "attn2.kv", (long)(n_req + 1) * L);
+        if (!dry && !err) {
+          AttnArgs a;
+          memset(&a, 0, sizeof(a));
+          const long kld = vt ? C : 2 * C;
+          a.q = q; a.q_ld = C; a.q_img = (long)hw * C;
+          a.k = ckv; a.k_ld = kld; a.k_img = (long)L * kld;
+          if (vt) {
+            a.v = cvt; a.v_ld = Lp; a.v_img = (long)C * Lp; a.vt = 1;
+          } else {
+            a.v = at(ckv, C); a.v_ld = kld; a.v_img = (long)L * kld;
+          }
+          a.kv_index = row_ctx;
+          a.o = x; a.o_ld = C; a.o_img = (long)hw * C;
+          a.imgs = rows; a.heads = t.heads; a.d = t.d; a.Nq = hw; a.Nk = L;
+          a.scale = 1.0f / sqrtf((float)t.d);
+          ok(launch_attention(h->dt, a, s), "cross-attention", K_ATTN, 4.0 * rows * hw * (double)L * C,
+             (2.0 * T * C + 2.0 * (n_req + 1) * L * C) * h->esz);
+        }
       }
       gemm(lin(x, C, T), nullptr, W(b.o2w), C, epi(z, C, Wf(b.o2b), z, C), "attn2.out", T);
       if (!dry && !err) ok(launch_layernorm(h->dt, z, x, T, C, Wf(b.ln3g), Wf(b.ln3b), 1e-5f, s), "ln3", K_LN, 8.0 * T * C, 2.0 * T * C * h->esz);

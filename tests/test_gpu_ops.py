@@ -86,16 +86,18 @@ def test_conv(ops, dt, case):
         assert err <= TOL[dt], (i, err)
 
 
+@pytest.mark.parametrize("vt", [False, True])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("heads,d,nq,nk,scale,cross", [
     (2, 8, 70, 70, 1.0, False), (2, 16, 33, 8, 1.0, True), (4, 32, 200, 200, 1.0, False),
     (8, 40, 300, 300, 1.0, False), (8, 40, 129, 77, 1.0, True), (2, 64, 256, 256, 30.0, False),
     (8, 80, 160, 160, 1.0, False), (8, 160, 64, 64, 1.0, False), (8, 160, 90, 77, 1.0, True),
+    (2, 40, 36, 36, 1.0, False),
 ])
-def test_attention(ops, dt, heads, d, nq, nk, scale, cross):
-    if dt == "f32" and d > 64:
-        pytest.skip("fp32 attention covers head widths <= 64")
-    log(f"attention {dt} heads={heads} d={d} nq={nq} nk={nk} x{scale} cross={cross}")
+def test_attention(ops, dt, vt, heads, d, nq, nk, scale, cross):
+    if dt == "f32" and (d > 64 or vt):
+        pytest.skip("fp32 attention covers head widths <= 64 with row-major V")
+    log(f"attention {dt} vt={vt} heads={heads} d={d} nq={nq} nk={nk} x{scale} cross={cross}")
     rng = np.random.default_rng(d * 1000 + nq)
     C = heads * d
     n = 3
@@ -105,8 +107,15 @@ def test_attention(ops, dt, heads, d, nq, nk, scale, cross):
     v = _vals(rng, (nkv, nk, C), dt)
     idx = np.array([1, 0, 1], np.int32) if cross else None
     o = torch.empty(n, nq, C, device="cuda", dtype=_tdt(dt))
-    ops.attention(_dev(q, dt), _dev(k, dt), _dev(v, dt), o, n, heads, d, nq, nk, C, C, C, nq * C, nk * C,
-                  nq * C, 1.0 / math.sqrt(d), kv_index=_dev(idx) if cross else None)
+    if vt:  # channel-major V with a padded token stride, as the step stores it
+        ld = (nk + 7) // 8 * 8
+        vdev = torch.zeros(nkv, C, ld, device="cuda", dtype=_tdt(dt))
+        vdev[:, :, :nk] = _dev(v, dt).transpose(1, 2)
+        v_ld, v_img = ld, C * ld
+    else:
+        vdev, v_ld, v_img = _dev(v, dt), C, nk * C
+    ops.attention(_dev(q, dt), _dev(k, dt), vdev, o, n, heads, d, nq, nk, C, nq * C, C, nk * C, v_ld, v_img,
+                  C, nq * C, 1.0 / math.sqrt(d), kv_index=_dev(idx) if cross else None, v_transposed=vt)
     torch.cuda.synchronize()
     got = o.float().cpu().numpy()
     for i in range(n):
