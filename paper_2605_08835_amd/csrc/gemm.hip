@@ -154,6 +154,61 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
+// The MFMAs compute C^T tiles (weights as the first operand), so element r
+// of lane l is (output channel 8*(r/4) + 4*(l/32) + r%4, pixel l%32): each
+// lane owns runs of 4 consecutive channels of one pixel and stores them with
+// one 8-byte (bf16) or 16-byte (fp32) write.  Tiles are visited with
+// compile-time indices so the accumulators stay in registers.
+template <int BM, int BN, int WM, int WN, int TM, int TN>
+__device__ __forceinline__ void epilogue_tiles(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int m0, int n0,
+                                               int wm, int wn, int lane) {
+  const int lr = lane & 31, hq = 4 * (lane >> 5);
+  static_for<0, TM>([&](auto I) {
+    static_for<0, TN>([&](auto J) {
+      const f32x16 v = acc[I.value][J.value];
+      const int m = m0 + wm * (BM / WM) + I.value * 32 + lr;
+      const int nt = n0 + wn * (BN / WN) + J.value * 32;
+      if (m < a.M) {
+        if (a.epi.geglu) {
+          // packed columns 32t + u (a) and 32t + 16 + u (gate) -> channel 16t + u
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            const int n = nt + 8 * q + hq;
+            if (n < a.N) {
+              float x[4], g[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                x[e] = v[4 * q + e] + a.epi.bias[n + e];
+                g[e] = v[4 * (q + 2) + e] + a.epi.bias[n + 16 + e];
+                x[e] *= 0.5f * g[e] * (1.0f + erff(g[e] * 0.70710678118654752f));
+              }
+              store4<bf16>(a.epi, m, nt / 2 + 8 * q + hq, x);
+            }
+          }
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int n = nt + 8 * q + hq;
+            if (n < a.N) {
+              float x[4] = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+              if (a.epi.vt_out && n >= a.epi.vt_col0) {
+                // transposed store: lanes l and l+1 hold consecutive tokens
+                const int img = m / a.epi.vt_hw, tok = m - img * a.epi.vt_hw;
+                bf16* o = reinterpret_cast<bf16*>(a.epi.vt_out) + (long)img * a.epi.vt_img +
+                          (long)(n - a.epi.vt_col0) * a.epi.vt_ld + tok;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[(long)e * a.epi.vt_ld] = (bf16)x[e];
+              } else {
+                epilogue4<bf16>(a.epi, m, n, x);
+              }
+            }
+          }
+        }
+      }
+    });
+  });
+}
+
 // Loader modes.
 //  0: per-thread addressing of any layer (incl. the GroupNorm affine on load).
 //  1: every segment is a stride-1 3x3 or 1x1 layer on an image of the
@@ -362,59 +417,206 @@ __global__ __launch_bounds__(256, MINB) void gemm_bf16_kernel(GemmArgs a) {
     __syncthreads();
   }
 
-  // The MFMAs compute C^T tiles (weights as the first operand), so element
-  // r of lane l is (output channel 8*(r/4) + 4*(l/32) + r%4, pixel l%32):
-  // each lane owns runs of 4 consecutive channels of one pixel and stores
-  // them with one 8-byte (bf16) or 16-byte (fp32) write.  Tiles are visited
-  // with compile-time indices so the accumulators stay in registers.
-  const int hq = 4 * (lane >> 5);
-  static_for<0, TM>([&](auto I) {
-    static_for<0, TN>([&](auto J) {
-      const f32x16 v = acc[I.value][J.value];
-      const int m = m0 + wm * (BM / WM) + I.value * 32 + lr;
-      const int nt = n0 + wn * (BN / WN) + J.value * 32;
-      if (m < a.M) {
-        if (a.epi.geglu) {
-          // packed columns 32t + u (a) and 32t + 16 + u (gate) -> channel 16t + u
-#pragma unroll
-          for (int q = 0; q < 2; ++q) {
-            const int n = nt + 8 * q + hq;
-            if (n < a.N) {
-              float x[4], g[4];
-#pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                x[e] = v[4 * q + e] + a.epi.bias[n + e];
-                g[e] = v[4 * (q + 2) + e] + a.epi.bias[n + 16 + e];
-                x[e] *= 0.5f * g[e] * (1.0f + erff(g[e] * 0.70710678118654752f));
-              }
-              store4<bf16>(a.epi, m, nt / 2 + 8 * q + hq, x);
-            }
-          }
-        } else {
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int n = nt + 8 * q + hq;
-            if (n < a.N) {
-              float x[4] = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
-              if (a.epi.vt_out && n >= a.epi.vt_col0) {
-                // transposed store: lanes l and l+1 hold consecutive tokens
-                const int img = m / a.epi.vt_hw, tok = m - img * a.epi.vt_hw;
-                bf16* o = reinterpret_cast<bf16*>(a.epi.vt_out) + (long)img * a.epi.vt_img +
-                          (long)(n - a.epi.vt_col0) * a.epi.vt_ld + tok;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) o[(long)e * a.epi.vt_ld] = (bf16)x[e];
-              } else {
-                epilogue4<bf16>(a.epi, m, n, x);
-              }
-            }
-          }
-        }
-      }
-    });
-  });
+  epilogue_tiles<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane);
 }
 
 
+
+
+// ------------------------------------------------- bf16 MFMA, direct-to-LDS
+// Same tiles and C^T epilogue as above, for the uniform-tap loader modes
+// (1, 2), with the operand tiles fetched by buffer_load ... lds: each 64-lane
+// load writes 1 KB of LDS contiguously (lane l at byte 16 l), so the loads
+// need no registers and three K stages stay in flight.  A tile row holds the
+// four 16-byte chunks of a 32-deep K slice; chunk c of row r sits in slot
+// c ^ ((r >> 2) & 3), which keeps the fragment reads of 8 consecutive rows
+// on distinct banks.  Lane l of a load writes (row 16 i + l / 4, slot l % 4)
+// and therefore fetches chunk (l % 4) ^ ((row >> 2) & 3) from global memory.
+constexpr int DK = 32, DNS = 3;  // K depth per stage, stages
+
+// One 16-byte-per-lane direct-to-LDS load (64 lanes -> 1 KB at `lds`).
+// The builtin exists only for the device pass; the host pass of this file
+// compiles the kernels' launch stubs and never runs this body.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, bf16* lds, int off) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, off, 0, 0, 0);
+#endif
+}
+
+template <int WAITN>
+__device__ __forceinline__ void wait_vmcnt() {
+  // s_waitcnt with only the vector-memory counter limited to WAITN
+  static_assert(WAITN >= 0 && WAITN < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((WAITN & 15) | (7 << 4) | (15 << 8) | ((WAITN >> 4) << 14));
+}
+
+template <int BM, int BN, int WM, int WN, int MODE>
+__global__ __launch_bounds__(256, 2) void gemm_bf16_dma_kernel(GemmArgs a) {
+  constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
+  constexpr int AI = BM / 16, BI = BN / 16;             // 1 KB loads per tile
+  constexpr int AW = AI / 4, BW = (BI + 3) / 4;         // ... per wave (B: some waves one fewer)
+  constexpr int LPT_MIN = AW + BI / 4;                  // loads per tile of the lightest wave
+  static_assert(AI % 4 == 0, "A tile must split evenly over 4 waves");
+  __shared__ __attribute__((aligned(1024))) bf16 As[DNS][BM * DK];
+  __shared__ __attribute__((aligned(1024))) bf16 Bs[DNS][BN * DK];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int tiles_n = (a.N + BN - 1) / BN;
+  int bid = blockIdx.x;
+  const int nb = gridDim.x;
+  if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
+  const int tm = bid / tiles_n, tn = bid - tm * tiles_n;
+  const int m0 = tm * BM, n0 = tn * BN;
+
+  // Rows and chunks this lane fetches: A load j of this wave is tile load
+  // i = wave * AW + j (rows 16 i ..); B load j is i = wave + 4 j.
+  const int lrow = lane >> 2, lslot = lane & 3;
+  const int Ho = a.seg[0].Ho, Wo = a.seg[0].Wo, hwo = Ho * Wo;
+  int ra0[AW], ra1[AW], achunk[AW];
+#pragma unroll
+  for (int j = 0; j < AW; ++j) {
+    const int r = 16 * (wave * AW + j) + lrow;
+    const int m = m0 + r;
+    achunk[j] = lslot ^ ((r >> 2) & 3);
+    if constexpr (MODE == 1) {
+      const int p = m % hwo, oy = p / Wo, ox = p - oy * Wo;
+      int mk = 0;
+#pragma unroll
+      for (int t = 0; t < 9; ++t) {
+        const int iy = oy + t / 3 - 1, ix = ox + t % 3 - 1;
+        if (iy >= 0 && iy < Ho && ix >= 0 && ix < Wo) mk |= 1 << t;
+      }
+      ra0[j] = m;
+      ra1[j] = m < a.M ? mk : 0;
+    } else {
+      const int img = m / hwo, p = m - img * hwo, oy = p / Wo, ox = p - oy * Wo;
+      ra0[j] = img * a.seg[0].Hi * a.seg[0].Wi;
+      ra1[j] = m < a.M ? (oy << 16) | ox : -1;
+    }
+  }
+  const __amdgpu_buffer_rsrc_t bres = make_rsrc(a.B, (long)a.N * a.ldb * 2);
+  int boff[BW];
+#pragma unroll
+  for (int j = 0; j < BW; ++j) {
+    const int i = wave + 4 * j;
+    const int r = 16 * i + lrow;
+    const int n = n0 + r;
+    const int c = lslot ^ ((r >> 2) & 3);
+    boff[j] = (i < BI && n < a.N) ? n * a.ldb * 2 + c * 16 : OOB;
+  }
+
+  int st_seg = 0, st_tap = 0, st_cb = 0;
+  // Issue the loads of K tile kt into stage `stg` (tiles are issued in order).
+  auto issue = [&](int kt, int stg) {
+    const int k0 = kt * DK;
+    const bool s1 = MODE == 1 && st_seg;
+    const int gcin = s1 ? a.seg[1].cin : a.seg[0].cin, gks = s1 ? a.seg[1].ks : a.seg[0].ks;
+    const int gc0 = s1 ? a.seg[1].c0 : a.seg[0].c0, gc1 = s1 ? a.seg[1].c1 : a.seg[0].c1;
+    const void* gs0 = s1 ? a.seg[1].src0 : a.seg[0].src0;
+    const void* gs1 = s1 ? a.seg[1].src1 : a.seg[0].src1;
+    const int tap = st_tap, cb = st_cb;
+    st_cb += DK;
+    if (st_cb >= gcin) {
+      st_cb = 0;
+      if (++st_tap == gks * gks) {
+        st_tap = 0;
+        st_seg = 1;
+      }
+    }
+    const bool in0 = cb < gc0;
+    const int cs = in0 ? gc0 : gc1, cbase = 2 * (in0 ? cb : cb - gc0);
+    bf16* adst = &As[stg][0];
+    if constexpr (MODE == 1) {
+      const __amdgpu_buffer_rsrc_t ares = make_rsrc(in0 ? gs0 : gs1, (long)a.M * cs * 2);
+      const int t9 = gks == 3 ? tap : 4;
+      const int dpix = gks == 3 ? (tap / 3 - 1) * Wo + (tap % 3 - 1) : 0;
+#pragma unroll
+      for (int j = 0; j < AW; ++j) {
+        const bool ok = (ra1[j] >> t9) & 1;
+        const int off = ok ? (ra0[j] + dpix) * cs * 2 + cbase + achunk[j] * 16 : OOB;
+        dma16(ares, adst + (wave * AW + j) * 512, off);
+      }
+    } else {
+      const ASeg& g = a.seg[0];
+      const long npix = (long)(a.M / hwo) * g.Hi * g.Wi;
+      const __amdgpu_buffer_rsrc_t ares = make_rsrc(gs0, npix * cs * 2);
+      const int ky = tap / 3 - 1, kx = tap % 3 - 1;
+#pragma unroll
+      for (int j = 0; j < AW; ++j) {
+        const int oy = ra1[j] >> 16, ox = ra1[j] & 0xFFFF;
+        int iy, ix;
+        bool ok;
+        if (g.up) {
+          iy = oy + ky;
+          ix = ox + kx;
+          ok = iy >= 0 && iy < 2 * g.Hi && ix >= 0 && ix < 2 * g.Wi;
+          iy >>= 1;
+          ix >>= 1;
+        } else {
+          iy = oy * g.stride + ky;
+          ix = ox * g.stride + kx;
+          ok = iy >= 0 && iy < g.Hi && ix >= 0 && ix < g.Wi;
+        }
+        ok = ok && ra1[j] >= 0;
+        const int off = ok ? (ra0[j] + iy * g.Wi + ix) * cs * 2 + cbase + achunk[j] * 16 : OOB;
+        dma16(ares, adst + (wave * AW + j) * 512, off);
+      }
+    }
+    bf16* bdst = &Bs[stg][0];
+#pragma unroll
+    for (int j = 0; j < BW; ++j) {
+      const int i = wave + 4 * j;
+      if (i < BI)  // wave-uniform
+        dma16(bres, bdst + i * 512, boff[j] == OOB ? OOB : boff[j] + 2 * k0);
+    }
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int nk = (a.K + DK - 1) / DK;  // K is a multiple of DK in modes 1, 2
+  issue(0, 0);
+  if (nk > 1) issue(1, 1);
+  const int lr = lane & 31, lh = lane >> 5;
+  const int arow = wm * (BM / WM) + lr, brow = wn * (BN / WN) + lr;
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + 1 < nk)
+      wait_vmcnt<LPT_MIN>();  // tile kt landed; tile kt+1 may still be in flight
+    else
+      wait_vmcnt<0>();
+    asm volatile("" ::: "memory");  // the LDS was written behind the compiler's back
+    __syncthreads();
+    if (kt + 2 < nk) issue(kt + 2, (kt + 2) % DNS);
+    const bf16* Ab = As[kt % DNS];
+    const bf16* Bb = Bs[kt % DNS];
+#pragma unroll
+    for (int ks = 0; ks < DK / 16; ++ks) {
+      const int ch = 2 * ks + lh;
+      bf16x8 af[TM], bfr[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int r = arow + i * 32;
+        af[i] = *reinterpret_cast<const bf16x8*>(&Ab[r * DK + 8 * (ch ^ ((r >> 2) & 3))]);
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int r = brow + j * 32;
+        bfr[j] = *reinterpret_cast<const bf16x8*>(&Bb[r * DK + 8 * (ch ^ ((r >> 2) & 3))]);
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+    }
+  }
+  epilogue_tiles<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane);
+}
 
 // ---------------------------------------------------------------- fp32 SIMT
 namespace sf {
@@ -524,6 +726,21 @@ static void launch_bf16(const GemmArgs& a, hipStream_t s) {
   }
 }
 
+// Direct-to-LDS kernel for the uniform-tap modes; false if the layer needs
+// the register-staged loader.
+template <int BM, int BN, int WM, int WN>
+static bool launch_dma(const GemmArgs& a, hipStream_t s) {
+  const int mode = loader_mode(a, DK);
+  if (mode == 0) return false;
+  const long blocks = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  const dim3 g((unsigned)blocks), b(256);
+  if (mode == 1)
+    gemm_bf16_dma_kernel<BM, BN, WM, WN, 1><<<g, b, 0, s>>>(a);
+  else
+    gemm_bf16_dma_kernel<BM, BN, WM, WN, 2><<<g, b, 0, s>>>(a);
+  return true;
+}
+
 // Tile choice: the widest N tile that divides N (320 and 160 cover every
 // SD-1.5 / SDXL width: 320, 640, 1280 and their 2x, 3x, 4x, 8x), then the
 // tallest M tile that still gives every CU about two blocks.  The choice
@@ -541,16 +758,15 @@ hipError_t launch_gemm(DType dt, const GemmArgs& a, hipStream_t s) {
     auto nblk = [&](int bm, int bn) { return (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn); };
     const long want = 2 * 256;
     if (a.N % 160 == 0) {
-      // 256x160 tiles, BK 32, two blocks per CU (acc in VGPRs, 2 waves/SIMD)
-      // when the loader is uniform; otherwise 64-deep tiles, one block per CU.
-      if (nblk(256, 160) >= want && loader_mode(a, 32) != 0)
-        launch_bf16<256, 160, 32, 4, 1, 2>(a, s);
-      else if (nblk(256, 160) >= want)
+      // 256x160 tiles through the direct-to-LDS pipeline when the loader is
+      // uniform; otherwise register-staged 64-deep tiles, one block per CU.
+      const bool big = nblk(256, 160) >= want;
+      if (big ? launch_dma<256, 160, 4, 1>(a, s) : launch_dma<128, 160, 4, 1>(a, s)) {
+      } else if (big) {
         launch_bf16<256, 160, 64, 4, 1>(a, s);
-      else if (loader_mode(a, 32) != 0)
-        launch_bf16<128, 160, 32, 4, 1, 2>(a, s);
-      else
+      } else {
         launch_bf16<128, 160, 64, 4, 1>(a, s);
+      }
     } else if (a.N % 128 == 0 || a.N > 64) {
       if (nblk(256, 128) >= want)
         launch_bf16<256, 128, 64, 2, 2>(a, s);

@@ -49,6 +49,13 @@ CONV_CASES = [
     (2, 9, 7, 40, 24, 136, 1, 1, 0, False),
     (1, 20, 20, 8, 0, 320, 3, 1, 0, False),
     (3, 8, 8, 320, 0, 4, 3, 1, 0, True),
+    # widths that take the direct-to-LDS pipeline (N % 160, cin % 32), ragged M
+    (3, 10, 9, 64, 0, 160, 3, 1, 0, False),
+    (2, 8, 8, 64, 96, 320, 3, 1, 0, False),
+    (2, 12, 12, 160, 0, 160, 3, 2, 0, False),
+    (2, 5, 7, 160, 0, 320, 3, 1, 1, False),
+    (2, 9, 7, 64, 32, 160, 1, 1, 0, False),
+    (64, 16, 16, 64, 0, 160, 3, 1, 0, False),
 ]
 
 
