@@ -15,4 +15,5 @@ name), so values do not depend on generation order or on the NumPy version.
 from .rng import Stream, bf16_round  # noqa: F401
 from .configs import CONFIGS, get_config, heads_of  # noqa: F401
 from .manifest import manifest, param_count  # noqa: F401
-from .synth import make_weights, make_requests, schedule_name  # noqa: F401
+from .synth import (make_weights, make_requests, schedule_name, serve_arrivals,  # noqa: F401
+                    serve_request_inputs, serve_null_context)

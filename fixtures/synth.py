@@ -4,6 +4,8 @@ Stream ids: weights 0, latents 1, cond context 2, uncond context 3,
 timesteps 4, Skip-CFG choice 5, guidance 6, arrivals 7, step counts 8,
 pooled embeddings 9.
 """
+import math
+
 import numpy as np
 
 from .configs import CONFIGS
@@ -99,3 +101,54 @@ def make_requests(workload, n_req=None):
         req["pooled_uncond"] = _maybe_bf16(pooled[R * P:], unet).reshape(P)
         req["time_ids"] = np.array(TIME_IDS, np.float32)
     return req
+
+
+def _poisson(u, lam):
+    """Poisson(lam) sample by inversion of the CDF at the uniform u."""
+    k, p = 0, math.exp(-lam)
+    c = p
+    while u > c and k < 1000:
+        k += 1
+        p *= lam / k
+        c += p
+    return k
+
+
+def serve_arrivals(workload, iterations):
+    """Arrival trace of the serving-loop workload: for each iteration the
+    list of (request id, denoising steps S_r, guidance w_r) that arrive.
+    Poisson(rate) arrivals per iteration, S_r uniform on the steps range,
+    w_r uniform on the guidance range."""
+    spec = CONFIGS[workload]
+    lam = spec["arrival_rate"]
+    lo, hi = spec["steps_range"]
+    g = spec["guidance"]
+    u = Stream(workload, 7).uniform(iterations)
+    counts = [_poisson(float(x), lam) for x in u]
+    total = sum(counts)
+    steps = Stream(workload, 8).integers(lo, hi + 1, total)
+    w = g[1] + (g[2] - g[1]) * Stream(workload, 6).uniform(total)
+    out, rid = [], 0
+    for c in counts:
+        batch = []
+        for _ in range(c):
+            batch.append((rid, int(steps[rid]), float(w[rid])))
+            rid += 1
+        out.append(batch)
+    return out
+
+
+def serve_request_inputs(workload, rid):
+    """Initial latent (C, H, W) and text context (L, D) of request `rid`."""
+    unet = CONFIGS[workload]["unet"]
+    C, H, W = unet["latent_c"], unet["latent_h"], unet["latent_w"]
+    L, D = unet["ctx_len"], unet["ctx_dim"]
+    lat = Stream(workload, 1, f"req{rid}").normal(C * H * W).reshape(C, H, W)
+    ctx = _maybe_bf16(Stream(workload, 2, f"req{rid}").normal(L * D), unet).reshape(L, D)
+    return lat.astype(np.float32), ctx
+
+
+def serve_null_context(workload):
+    unet = CONFIGS[workload]["unet"]
+    return _maybe_bf16(Stream(workload, 3).normal(unet["ctx_len"] * unet["ctx_dim"]), unet).reshape(
+        unet["ctx_len"], unet["ctx_dim"])

@@ -90,6 +90,12 @@ def test_c3_full_size_sampled(weights_cache):
     check("c3_sd15_mixed32", weights_cache, only=[on, off], req=req)
 
 
+def test_c4_sdxl_full_size_sampled(weights_cache):
+    """SDXL-like UNet at 128x128 (8 requests with CFG, 16 rows): the full
+    batch runs on the GPU; request 3 is recomputed by the oracle."""
+    check("c4_sdxl_cfg8", weights_cache, only=[3])
+
+
 def test_batch_permutation_is_bitwise_invariant(weights_cache):
     wl = "t_sd15_16"
     req = make_requests(wl)
