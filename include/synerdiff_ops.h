@@ -30,13 +30,20 @@ extern "C" {
  * when upsampling.  w is the packed weight [cout, ks*ks*cin] (tap-major,
  * channel-minor).  bias may be NULL; resid ([n, Ho, Wo, cout], activation
  * dtype) may be NULL or equal to out.  out_f32 = 1 writes fp32 output.
+ * d_scratch (fp32, scratch_floats long, may be NULL) lets the call split K
+ * the way the step does for long-K 3x3 layers on small images (ks = 1 never
+ * splits);
+ * synerdiff_op_conv_scratch_floats returns the floats that needs (0 = no
+ * split for this shape).
  * Constraints: ks in {1, 3}; stride in {1, 2}; c0, c1 multiples of 8;
  * bf16: cout a multiple of 4. */
 sd_status synerdiff_op_conv(int32_t dtype, const void* d_x0, int32_t c0, const void* d_x1, int32_t c1,
                             int32_t n, int32_t H, int32_t W, int32_t ks, int32_t stride, int32_t up,
                             const float* d_scale, const float* d_shift, int32_t silu, const void* d_w,
                             int32_t cout, const float* d_bias, const void* d_resid, void* d_out,
-                            int32_t out_f32, void* hip_stream);
+                            int32_t out_f32, float* d_scratch, int64_t scratch_floats, void* hip_stream);
+int64_t synerdiff_op_conv_scratch_floats(int32_t dtype, int32_t c0, int32_t c1, int32_t n, int32_t H, int32_t W,
+                                         int32_t ks, int32_t stride, int32_t up, int32_t cout);
 
 /* Multi-head attention O = softmax(Q K^T * scale) V per image and head
  * (head h uses channels [h*d, (h+1)*d)).  Q: image i, token t, channel c at

@@ -61,7 +61,9 @@ _SIG = {
     "synerdiff_profile_read": (ctypes.c_int, [_P, ctypes.POINTER(KernelStat), ctypes.c_int32,
                                               ctypes.POINTER(ctypes.c_int32), ctypes.c_int32]),
     "synerdiff_op_conv": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, _P] + [ctypes.c_int32] * 7 +
-                          [_P, _P, ctypes.c_int32, _P, ctypes.c_int32, _P, _P, _P, ctypes.c_int32, _P]),
+                          [_P, _P, ctypes.c_int32, _P, ctypes.c_int32, _P, _P, _P, ctypes.c_int32, _P,
+                           ctypes.c_int64, _P]),
+    "synerdiff_op_conv_scratch_floats": (ctypes.c_int64, [ctypes.c_int32] * 10),
     "synerdiff_op_attention": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int64, ctypes.c_int64, _P,
                                               ctypes.c_int64, ctypes.c_int64, _P, ctypes.c_int64, ctypes.c_int64,
                                               ctypes.c_int32, _P, _P, ctypes.c_int64, ctypes.c_int64] +

@@ -432,7 +432,7 @@ __global__ __launch_bounds__(256, MINB) void gemm_bf16_kernel(GemmArgs a) {
 // c ^ ((r >> 2) & 3), which keeps the fragment reads of 8 consecutive rows
 // on distinct banks.  Lane l of a load writes (row 16 i + l / 4, slot l % 4)
 // and therefore fetches chunk (l % 4) ^ ((row >> 2) & 3) from global memory.
-constexpr int DK = 32, DNS = 3;  // K depth per stage, stages
+constexpr int DK = 32;  // K depth per stage
 
 // One 16-byte-per-lane direct-to-LDS load (64 lanes -> 1 KB at `lds`).
 // The builtin exists only for the device pass; the host pass of this file
@@ -450,12 +450,13 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((WAITN & 15) | (7 << 4) | (15 << 8) | ((WAITN >> 4) << 14));
 }
 
-template <int BM, int BN, int WM, int WN, int MODE>
-__global__ __launch_bounds__(256, 2) void gemm_bf16_dma_kernel(GemmArgs a) {
+template <int BM, int BN, int WM, int WN, int MODE, int DNS, int MINB>
+__global__ __launch_bounds__(256, MINB) void gemm_bf16_dma_kernel(GemmArgs a) {
   constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
   constexpr int AI = BM / 16, BI = BN / 16;             // 1 KB loads per tile
   constexpr int AW = AI / 4, BW = (BI + 3) / 4;         // ... per wave (B: some waves one fewer)
   constexpr int LPT_MIN = AW + BI / 4;                  // loads per tile of the lightest wave
+  static_assert(DNS >= 2 && DNS <= 4, "pipeline depth");
   static_assert(AI % 4 == 0, "A tile must split evenly over 4 waves");
   __shared__ __attribute__((aligned(1024))) bf16 As[DNS][BM * DK];
   __shared__ __attribute__((aligned(1024))) bf16 Bs[DNS][BN * DK];
@@ -465,6 +466,9 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_dma_kernel(GemmArgs a) {
   int bid = blockIdx.x;
   const int nb = gridDim.x;
   if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
+  // split-K: blocks split * tiles .. cover K tiles [kb, ke) of their output tile
+  const int tiles = (nb / a.ksplit), split = bid / tiles;
+  bid -= split * tiles;
   const int tm = bid / tiles_n, tn = bid - tm * tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
 
@@ -505,7 +509,20 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_dma_kernel(GemmArgs a) {
     boff[j] = (i < BI && n < a.N) ? n * a.ldb * 2 + c * 16 : OOB;
   }
 
+  const int nk_all = (a.K + DK - 1) / DK;  // K is a multiple of DK in modes 1, 2
+  const int per = (nk_all + a.ksplit - 1) / a.ksplit;
+  const int kb = split * per, ke = min(nk_all, kb + per);
   int st_seg = 0, st_tap = 0, st_cb = 0;
+  {  // loader state at K tile kb
+    int kk = kb * DK;
+    if (MODE == 1 && kk >= a.seg[0].K) {
+      st_seg = 1;
+      kk -= a.seg[0].K;
+    }
+    const int gcin = st_seg ? a.seg[1].cin : a.seg[0].cin;
+    st_tap = kk / gcin;
+    st_cb = kk - st_tap * gcin;
+  }
   // Issue the loads of K tile kt into stage `stg` (tiles are issued in order).
   auto issue = [&](int kt, int stg) {
     const int k0 = kt * DK;
@@ -579,19 +596,25 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_dma_kernel(GemmArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int nk = (a.K + DK - 1) / DK;  // K is a multiple of DK in modes 1, 2
-  issue(0, 0);
-  if (nk > 1) issue(1, 1);
+  const int nk = ke - kb;
+#pragma unroll
+  for (int p = 0; p < DNS - 1; ++p)
+    if (p < nk) issue(kb + p, p);
   const int lr = lane & 31, lh = lane >> 5;
   const int arow = wm * (BM / WM) + lr, brow = wn * (BN / WN) + lr;
   for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk)
-      wait_vmcnt<LPT_MIN>();  // tile kt landed; tile kt+1 may still be in flight
+    // Tile kt must have landed; the tiles issued after it may still be in
+    // flight (at most DNS-2 of them, fewer near the end of K).
+    const int ahead = min(DNS - 2, nk - 1 - kt);
+    if (ahead >= 2)
+      wait_vmcnt<2 * LPT_MIN>();
+    else if (ahead == 1)
+      wait_vmcnt<LPT_MIN>();
     else
       wait_vmcnt<0>();
     asm volatile("" ::: "memory");  // the LDS was written behind the compiler's back
     __syncthreads();
-    if (kt + 2 < nk) issue(kt + 2, (kt + 2) % DNS);
+    if (kt + DNS - 1 < nk) issue(kb + kt + DNS - 1, (kt + DNS - 1) % DNS);
     const bf16* Ab = As[kt % DNS];
     const bf16* Bb = Bs[kt % DNS];
 #pragma unroll
@@ -615,7 +638,43 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_dma_kernel(GemmArgs a) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
     }
   }
+  if (a.ksplit > 1) {
+    // raw fp32 partial sums; the reduction kernel applies the epilogue
+    const int lr = lane & 31, hq = 4 * (lane >> 5);
+    float* P = a.partial + (long)split * a.M * a.N;
+    static_for<0, TM>([&](auto I) {
+      static_for<0, TN>([&](auto J) {
+        const f32x16 v = acc[I.value][J.value];
+        const int m = m0 + wm * (BM / WM) + I.value * 32 + lr;
+        const int nt = n0 + wn * (BN / WN) + J.value * 32;
+        if (m < a.M) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int n = nt + 8 * q + hq;
+            if (n < a.N)
+              *reinterpret_cast<float4*>(P + (long)m * a.N + n) =
+                  make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+          }
+        }
+      });
+    });
+    return;
+  }
   epilogue_tiles<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane);
+}
+
+// Sum of the split-K partials in split order, then the epilogue.
+__global__ void splitk_reduce_kernel(GemmArgs a) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;  // one run of 4 columns
+  const int nv = a.N / 4;
+  if (i >= (long)a.M * nv) return;
+  const int m = (int)(i / nv), n = (int)(i - (long)m * nv) * 4;
+  float x[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < a.ksplit; ++s) {
+    const float4 v = *reinterpret_cast<const float4*>(a.partial + ((long)s * a.M + m) * a.N + n);
+    x[0] += v.x; x[1] += v.y; x[2] += v.z; x[3] += v.w;
+  }
+  epilogue4<bf16>(a.epi, m, n, x);
 }
 
 // ---------------------------------------------------------------- fp32 SIMT
@@ -728,26 +787,49 @@ static void launch_bf16(const GemmArgs& a, hipStream_t s) {
 
 // Direct-to-LDS kernel for the uniform-tap modes; false if the layer needs
 // the register-staged loader.
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, int DNS, int MINB>
 static bool launch_dma(const GemmArgs& a, hipStream_t s) {
   const int mode = loader_mode(a, DK);
   if (mode == 0) return false;
-  const long blocks = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  const long blocks = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN) * a.ksplit;
   const dim3 g((unsigned)blocks), b(256);
   if (mode == 1)
-    gemm_bf16_dma_kernel<BM, BN, WM, WN, 1><<<g, b, 0, s>>>(a);
+    gemm_bf16_dma_kernel<BM, BN, WM, WN, 1, DNS, MINB><<<g, b, 0, s>>>(a);
   else
-    gemm_bf16_dma_kernel<BM, BN, WM, WN, 2><<<g, b, 0, s>>>(a);
+    gemm_bf16_dma_kernel<BM, BN, WM, WN, 2, DNS, MINB><<<g, b, 0, s>>>(a);
+  if (a.ksplit > 1) {
+    const long n = (long)a.M * (a.N / 4);
+    splitk_reduce_kernel<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s>>>(a);
+  }
   return true;
+}
+
+// Split-K factor of a bf16 GEMM: long-K 3x3 convolutions on the small
+// levels (16x16 and 8x8 images) have too few output tiles to fill 256 CUs.
+// The factor depends only on K and the per-image output size, never on the
+// number of rows, so a row's result does not depend on its batch-mates.
+// Linear layers (1x1, the row count as image width) are never split: their
+// "image" size is the row count.
+int gemm_ksplit(const GemmArgs& a) {
+  const long hw = (long)a.seg[0].Ho * a.seg[0].Wo;
+  if (a.seg[0].ks != 3 || a.K < 5120 || hw > 256 || a.N % 160 || a.epi.geglu || a.epi.vt_out || a.epi.out_f32)
+    return 1;
+  if (loader_mode(a, DK) == 0) return 1;
+  return hw <= 64 ? 4 : 2;
 }
 
 // Tile choice: the widest N tile that divides N (320 and 160 cover every
 // SD-1.5 / SDXL width: 320, 640, 1280 and their 2x, 3x, 4x, 8x), then the
-// tallest M tile that still gives every CU about two blocks.  The choice
-// depends on the layer shape and the row count only through M, and no K is
-// split, so a row's result never depends on its batch-mates.
-hipError_t launch_gemm(DType dt, const GemmArgs& a, hipStream_t s) {
+// tallest M tile that still gives every CU about two blocks.  The tile shape
+// never changes a row's K order, so only the split factor (a function of the
+// layer shape) decides a row's bits.
+hipError_t launch_gemm(DType dt, const GemmArgs& args, hipStream_t s) {
+  GemmArgs a = args;
+  if (a.ksplit < 1) a.ksplit = 1;
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  if (a.ksplit > 1 && (dt != BF16 || !a.partial || a.epi.geglu || a.epi.vt_out || a.epi.out_f32 ||
+                       a.N % 160 || loader_mode(a, DK) == 0))
+    return hipErrorInvalidValue;
   if (dt == BF16 && (a.N % 4 || a.epi.ldo % 4 || (a.epi.resid && a.epi.ldr % 4) || (a.epi.geglu && a.N % 32)))
     return hipErrorInvalidValue;
   if (dt != BF16 && (a.epi.geglu || a.epi.vt_out)) return hipErrorInvalidValue;
@@ -760,8 +842,8 @@ hipError_t launch_gemm(DType dt, const GemmArgs& a, hipStream_t s) {
     if (a.N % 160 == 0) {
       // 256x160 tiles through the direct-to-LDS pipeline when the loader is
       // uniform; otherwise register-staged 64-deep tiles, one block per CU.
-      const bool big = nblk(256, 160) >= want;
-      if (big ? launch_dma<256, 160, 4, 1>(a, s) : launch_dma<128, 160, 4, 1>(a, s)) {
+      const bool big = nblk(256, 160) * a.ksplit >= want;
+      if (big ? launch_dma<256, 160, 4, 1, 3, 2>(a, s) : launch_dma<128, 160, 4, 1, 3, 2>(a, s)) {
       } else if (big) {
         launch_bf16<256, 160, 64, 4, 1>(a, s);
       } else {

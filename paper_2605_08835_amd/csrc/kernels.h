@@ -54,10 +54,14 @@ struct GemmArgs {
   const void* B;     // packed weights [N, ldb], K contiguous, activation dtype
   int ldb;
   Epi epi;
+  int ksplit;        // >= 1; > 1: K split into ksplit ranges, fp32 partials in
+  float* partial;    //   partial[ksplit][M][N], summed in order by a second kernel
 };
 
 // bf16 requires N % 4 == 0, 8-byte aligned outputs and ldo, ldr % 4 == 0.
 hipError_t launch_gemm(DType dt, const GemmArgs& a, hipStream_t s);
+// Split-K factor launch_gemm supports for this bf16 GEMM (1 = no split).
+int gemm_ksplit(const GemmArgs& a);
 
 // Attention: O = softmax(Q K^T * scale) V per (img, head).
 struct AttnArgs {

@@ -25,20 +25,10 @@ static bool bad_dtype(int32_t d) { return d != SD_F32 && d != SD_BF16; }
 
 extern "C" {
 
-sd_status synerdiff_op_conv(int32_t dtype, const void* x0, int32_t c0, const void* x1, int32_t c1, int32_t n,
-                            int32_t H, int32_t W, int32_t ks, int32_t stride, int32_t up, const float* scale,
-                            const float* shift, int32_t silu, const void* w, int32_t cout, const float* bias,
-                            const void* resid, void* out, int32_t out_f32, void* stream) {
-  if (bad_dtype(dtype)) return op_fail(SD_ERR_INVALID_ARG, "bad dtype");
-  if (!x0 || !w || !out || (c1 && !x1) || (!scale) != (!shift)) return op_fail(SD_ERR_INVALID_ARG, "NULL argument");
-  if (n < 0 || H < 1 || W < 1 || c0 < 8 || c0 % 8 || c1 < 0 || c1 % 8 || cout < 1)
-    return op_fail(SD_ERR_INVALID_ARG, "bad shape");
-  if ((ks != 1 && ks != 3) || (stride != 1 && stride != 2) || (up && stride != 1) || (ks == 1 && (stride != 1 || up)))
-    return op_fail(SD_ERR_UNSUPPORTED, "unsupported ks/stride/up");
-  if (stride == 2 && (H % 2 || W % 2)) return op_fail(SD_ERR_UNSUPPORTED, "stride 2 needs even H, W");
-  if (dtype == SD_BF16 && cout % 4) return op_fail(SD_ERR_UNSUPPORTED, "bf16 needs cout % 4 == 0");
-  if (n == 0) return SD_OK;
-  GemmArgs a;
+static bool conv_args(int32_t dtype, const void* x0, int32_t c0, const void* x1, int32_t c1, int32_t n, int32_t H,
+                      int32_t W, int32_t ks, int32_t stride, int32_t up, const float* scale, const float* shift,
+                      int32_t silu, const void* w, int32_t cout, const float* bias, const void* resid, void* out,
+                      int32_t out_f32, GemmArgs& a) {
   memset(&a, 0, sizeof(a));
   ASeg& s = a.seg[0];
   s.src0 = x0; s.src1 = x1; s.c0 = c0; s.c1 = c1; s.cin = c0 + c1;
@@ -49,10 +39,52 @@ sd_status synerdiff_op_conv(int32_t dtype, const void* x0, int32_t c0, const voi
   s.Wo = up ? 2 * W : W / stride;
   s.K = ks * ks * s.cin;
   const long M = (long)n * s.Ho * s.Wo;
-  if (M > 0x7FFFFFFFL) return op_fail(SD_ERR_UNSUPPORTED, "too many output pixels");
+  if (M > 0x7FFFFFFFL) return false;
   a.M = (int)M; a.N = cout; a.K = s.K; a.B = w; a.ldb = s.K;
   a.epi.bias = bias; a.epi.resid = resid; a.epi.ldr = cout; a.epi.out = out; a.epi.ldo = cout;
   a.epi.out_f32 = out_f32 ? 1 : 0; a.epi.hw = 1;
+  a.ksplit = 1;
+  (void)dtype;
+  return true;
+}
+
+int64_t synerdiff_op_conv_scratch_floats(int32_t dtype, int32_t c0, int32_t c1, int32_t n, int32_t H, int32_t W,
+                                         int32_t ks, int32_t stride, int32_t up, int32_t cout) {
+  if (dtype != SD_BF16 || n <= 0 || H < 1 || W < 1 || c0 < 8 || cout < 1) return 0;
+  GemmArgs a;
+  static int dummy;
+  if (!conv_args(dtype, &dummy, c0, c1 ? &dummy : nullptr, c1, n, H, W, ks, stride, up, nullptr, nullptr, 0,
+                 &dummy, cout, nullptr, nullptr, &dummy, 0, a))
+    return 0;
+  const int ksplit = gemm_ksplit(a);
+  return ksplit > 1 ? (int64_t)ksplit * a.M * a.N : 0;
+}
+
+sd_status synerdiff_op_conv(int32_t dtype, const void* x0, int32_t c0, const void* x1, int32_t c1, int32_t n,
+                            int32_t H, int32_t W, int32_t ks, int32_t stride, int32_t up, const float* scale,
+                            const float* shift, int32_t silu, const void* w, int32_t cout, const float* bias,
+                            const void* resid, void* out, int32_t out_f32, float* scratch, int64_t scratch_floats,
+                            void* stream) {
+  if (bad_dtype(dtype)) return op_fail(SD_ERR_INVALID_ARG, "bad dtype");
+  if (!x0 || !w || !out || (c1 && !x1) || (!scale) != (!shift)) return op_fail(SD_ERR_INVALID_ARG, "NULL argument");
+  if (n < 0 || H < 1 || W < 1 || c0 < 8 || c0 % 8 || c1 < 0 || c1 % 8 || cout < 1)
+    return op_fail(SD_ERR_INVALID_ARG, "bad shape");
+  if ((ks != 1 && ks != 3) || (stride != 1 && stride != 2) || (up && stride != 1) || (ks == 1 && (stride != 1 || up)))
+    return op_fail(SD_ERR_UNSUPPORTED, "unsupported ks/stride/up");
+  if (stride == 2 && (H % 2 || W % 2)) return op_fail(SD_ERR_UNSUPPORTED, "stride 2 needs even H, W");
+  if (dtype == SD_BF16 && cout % 4) return op_fail(SD_ERR_UNSUPPORTED, "bf16 needs cout % 4 == 0");
+  if (n == 0) return SD_OK;
+  GemmArgs a;
+  if (!conv_args(dtype, x0, c0, x1, c1, n, H, W, ks, stride, up, scale, shift, silu, w, cout, bias, resid, out,
+                 out_f32, a))
+    return op_fail(SD_ERR_UNSUPPORTED, "too many output pixels");
+  if (dtype == SD_BF16 && scratch) {
+    const int ksplit = gemm_ksplit(a);
+    if (ksplit > 1 && scratch_floats >= (int64_t)ksplit * a.M * a.N) {
+      a.ksplit = ksplit;
+      a.partial = scratch;
+    }
+  }
   return op_hip(launch_gemm((DType)dtype, a, (hipStream_t)stream), "conv");
 }
 

@@ -77,7 +77,7 @@ struct LevelW {
 // Workspace roles (buffers sized by a dry run at max capacity).
 enum Role {
   R_X0, R_HA, R_HB, R_U, R_TZ, R_TX, R_TQ, R_TF, R_CTX, R_CKV, R_GNP, R_GNS, R_GNH,
-  R_E, R_A, R_H1, R_TAU, R_T2, R_TB, R_EPS, R_SCAL, R_GNA, R_TV, R_CVT, R_SKIP0
+  R_E, R_A, R_H1, R_TAU, R_T2, R_TB, R_EPS, R_SCAL, R_GNA, R_TV, R_CVT, R_SPLIT, R_SKIP0
 };
 
 }  // namespace sd
@@ -429,7 +429,7 @@ struct Step {
   // overrides the algorithmic K (conv_in's channel padding is not counted).
   void gemm(const ASeg& s0, const ASeg* s1, const void* B, int N, const Epi& e, const char* w, long M = -1,
             double kalg = -1) {
-    if (dry || err) return;
+    if (err) return;
     GemmArgs a;
     memset(&a, 0, sizeof(a));
     a.seg[0] = s0;
@@ -440,6 +440,9 @@ struct Step {
     a.B = B;
     a.ldb = a.K;
     a.epi = e;
+    a.ksplit = h->dt == BF16 ? gemm_ksplit(a) : 1;
+    if (a.ksplit > 1) a.partial = (float*)buf(R_SPLIT, (size_t)a.ksplit * a.M * N * 4);
+    if (dry) return;
     const double K = kalg > 0 ? kalg : a.K;
     const double es = h->esz, outb = e.out_f32 ? 4 : es;
     auto seg_bytes = [&](const ASeg& g, long m) {

@@ -18,15 +18,17 @@ def _s():
 
 
 def conv(x0, w_packed, cout, ks=3, stride=1, up=0, x1=None, scale=None, shift=None, silu=0, bias=None,
-         resid=None, out=None, out_f32=False):
+         resid=None, out=None, out_f32=False, split=True):
     n, H, W, c0 = x0.shape
     c1 = 0 if x1 is None else x1.shape[3]
     Ho, Wo = (2 * H, 2 * W) if up else (H // stride, W // stride)
     if out is None:
         out = torch.empty(n, Ho, Wo, cout, device=x0.device, dtype=torch.float32 if out_f32 else x0.dtype)
+    nsc = lib().synerdiff_op_conv_scratch_floats(_dt(x0), c0, c1, n, H, W, ks, stride, up, cout) if split else 0
+    scratch = torch.empty(nsc, device=x0.device) if nsc > 0 else None
     _check(lib().synerdiff_op_conv(_dt(x0), _ptr(x0), c0, _ptr(x1), c1, n, H, W, ks, stride, up, _ptr(scale),
                                    _ptr(shift), silu, _ptr(w_packed), cout, _ptr(bias), _ptr(resid), _ptr(out),
-                                   int(out_f32), _s()))
+                                   int(out_f32), _ptr(scratch), nsc, _s()))
     return out
 
 

@@ -125,3 +125,24 @@ def test_step_argument_validation_happens_before_any_gpu_work(lib):
     assert step(lat_=None) == -1
     assert "overlap" in lib.synerdiff_last_error().decode() or lib.synerdiff_last_error()
     lib.synerdiff_unet_destroy(h)
+
+
+def test_split_k_factor_depends_on_layer_shape_only(lib):
+    """The K split of a convolution is a function of the layer (K, per-image
+    size, width), never of the number of images, and linear (1x1) layers are
+    not split; this is what keeps a request's bits independent of its
+    batch-mates."""
+    f = lib.synerdiff_op_conv_scratch_floats
+    BF16 = 1
+    for (c0, c1, H, W, ks, stride, up, cout) in [(640, 0, 4, 4, 3, 1, 0, 320), (1280, 0, 8, 8, 3, 1, 0, 1280),
+                                                (1280, 1280, 8, 8, 3, 1, 0, 1280), (1280, 0, 16, 16, 3, 2, 0, 1280),
+                                                (1280, 0, 8, 8, 3, 1, 1, 1280), (320, 0, 32, 32, 3, 1, 0, 320)]:
+        Ho, Wo = (2 * H, 2 * W) if up else (H // stride, W // stride)
+        ks_per_n = {f(BF16, c0, c1, n, H, W, ks, stride, up, cout) // (n * Ho * Wo * cout) for n in (1, 2, 3, 7, 48)}
+        assert len(ks_per_n) == 1, (c0, H, ks_per_n)
+    assert f(BF16, 640, 0, 1, 8, 8, 3, 1, 0, 640) // (64 * 640) == 4      # K = 5760 on 8x8: split in 4
+    assert f(BF16, 640, 0, 1, 16, 16, 3, 1, 0, 640) // (256 * 640) == 2  # 16x16: split in 2
+    assert f(BF16, 320, 0, 1, 32, 32, 3, 1, 0, 320) == 0                 # short K: no split
+    for n in (1, 8, 64, 300):                                            # linear layers: rows as width
+        assert f(BF16, 5120, 0, 1, 1, n, 1, 1, 0, 1280) == 0
+    assert f(0, 640, 0, 1, 8, 8, 3, 1, 0, 640) == 0                      # fp32: no split

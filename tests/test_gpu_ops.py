@@ -56,6 +56,12 @@ CONV_CASES = [
     (2, 5, 7, 160, 0, 320, 3, 1, 1, False),
     (2, 9, 7, 64, 32, 160, 1, 1, 0, False),
     (64, 16, 16, 64, 0, 160, 3, 1, 0, False),
+    # long-K layers on small images: split K (ragged row counts)
+    (3, 4, 4, 640, 0, 320, 3, 1, 0, False),
+    (5, 2, 2, 1280, 0, 160, 3, 1, 0, False),
+    (2, 4, 4, 640, 640, 320, 3, 1, 0, False),
+    (3, 4, 4, 1280, 0, 160, 3, 2, 0, False),
+    (2, 2, 2, 640, 0, 320, 3, 1, 1, False),
 ]
 
 
@@ -182,3 +188,19 @@ def test_geglu(ops, dt):
     ref = xd[:, :320] * O.gelu(xd[:, 320:])
     err = rel_l2(y.float().cpu().numpy(), ref)
     assert err <= (2e-6 if dt == "f32" else 6e-3), err
+
+
+@pytest.mark.parametrize("n", [1, 3, 6])
+def test_conv_split_k_rows_independent(ops, n):
+    """The split-K path gives each image the same bits whatever the batch."""
+    rng = np.random.default_rng(21)
+    x = _vals(rng, (6, 4, 4, 640), "bf16")
+    w = _vals(rng, (320, 640, 3, 3), "bf16", 0.01)
+    wp = _dev(_pack(w), "bf16")
+    full = ops.conv(_dev(x, "bf16"), wp, 320).float().cpu().numpy()
+    part = ops.conv(_dev(x[:n], "bf16"), wp, 320).float().cpu().numpy()
+    nosplit = ops.conv(_dev(x[:n], "bf16"), wp, 320, split=False).float().cpu().numpy()
+    assert np.array_equal(full[:n], part)
+    err = rel_l2(part, nosplit)
+    log(f"split-K n={n}: rel L2 vs one pass {err:.2e}")
+    assert err < 1e-2
