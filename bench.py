@@ -68,6 +68,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layers", default=None, help="write a per-layer device-time table to this file")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the step shards by request with no collective, "
@@ -118,11 +119,20 @@ def main():
     # Per-kernel-class split: the same steps again with an event after every launch.
     m.profile(True)
     m.profile_read(reset=True)
+    m.profile_read_layers(reset=True)
     for _ in range(args.steps):
         step()
         m.profile_read(reset=False)
     prof = m.profile_read(reset=True)
+    layers = m.profile_read_layers(reset=True)
     m.profile(False)
+    if args.layers:
+        with open(args.layers, "w") as f:
+            f.write(f"{'layer':44s} {'launches':>8s} {'ms/step':>8s} {'us/launch':>10s} {'TFLOP/s':>8s} {'GB/s':>8s}\n")
+            for k, v in sorted(layers.items(), key=lambda kv: -kv[1]["ms"]):
+                n = v["launches"]
+                f.write(f"{k:44s} {n / args.steps:8.1f} {v['ms'] / args.steps:8.3f} {1e3 * v['ms'] / n:10.1f} "
+                        f"{v['flop'] / max(v['ms'], 1e-9) / 1e9:8.1f} {v['bytes'] / max(v['ms'], 1e-9) / 1e6:8.1f}\n")
     kernels = {}
     for k, v in prof.items():
         n = v["launches"]

@@ -166,6 +166,20 @@ typedef struct {
 } sd_kernel_stat;
 sd_status synerdiff_profile(sd_unet* h, int32_t enable);
 sd_status synerdiff_profile_read(sd_unet* h, sd_kernel_stat* out, int32_t cap, int32_t* n_out, int32_t reset);
+/* The same totals per layer instead of per class: one entry per distinct
+ * launch name ("conv1 196608x320x2880" = a GEMM named conv1 with M x N x K,
+ * "self-attention 4096x4096 d40" = query x key tokens and head width, other
+ * kernels by their step name), in first-launch order.  Same arguments and
+ * reset semantics as synerdiff_profile_read. */
+typedef struct {
+  char name[64];
+  int64_t launches;
+  double ms;
+  double flop;
+  double bytes;
+} sd_layer_stat;
+sd_status synerdiff_profile_read_layers(sd_unet* h, sd_layer_stat* out, int32_t cap, int32_t* n_out,
+                                        int32_t reset);
 
 void synerdiff_unet_destroy(sd_unet* h);
 

@@ -48,17 +48,20 @@ int64_t synerdiff_op_conv_scratch_floats(int32_t dtype, int32_t c0, int32_t c1, 
 /* Multi-head attention O = softmax(Q K^T * scale) V per image and head
  * (head h uses channels [h*d, (h+1)*d)).  Q: image i, token t, channel c at
  * q + i*q_img + t*q_ld + c; K likewise with k_img, k_ld and image
- * kv_index[i] (d_kv_index NULL = image i); V likewise with v_img, v_ld, or,
- * when v_transposed = 1 (bf16 only), at v + j*v_img + c*v_ld + t (channel-
- * major, the layout the step's projections write); O like Q with o_img,
- * o_ld.  Strides in elements.  Constraints: d a multiple of 8; bf16:
- * d <= 256 and not in (192, 224]; fp32: d <= 64. */
+ * kv_index[i] (d_kv_index NULL = image i); V likewise with v_img, v_ld
+ * (fp32), or, with v_transposed = 1 (required for bf16), at
+ * v + j*v_img + c*v_ld + t (channel-major, the layout the step's
+ * projections write); O like Q with o_img, o_ld.  Strides in elements.
+ * q_log2 = 1 (bf16 only): Q already holds q * scale * log2(e), as the
+ * step's projections write it (scale is then unused).  Constraints: d a
+ * multiple of 8; bf16: d rounded up to 16 is 16..96, 128, 160, 192 or 256;
+ * fp32: d <= 64. */
 sd_status synerdiff_op_attention(int32_t dtype, const void* d_q, int64_t q_ld, int64_t q_img,
                                  const void* d_k, int64_t k_ld, int64_t k_img, const void* d_v,
                                  int64_t v_ld, int64_t v_img, int32_t v_transposed,
                                  const int32_t* d_kv_index, void* d_o, int64_t o_ld, int64_t o_img,
                                  int32_t n, int32_t heads, int32_t d, int32_t n_q, int32_t n_k,
-                                 float scale, void* hip_stream);
+                                 float scale, int32_t q_log2, void* hip_stream);
 
 /* GroupNorm statistics of the concat [x0 | x1] ([n, hw, c0 + c1]) with
  * `groups` groups of consecutive channels, biased variance, eps: writes the

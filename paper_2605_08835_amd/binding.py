@@ -37,6 +37,11 @@ class KernelStat(ctypes.Structure):
                 ("flop", ctypes.c_double), ("bytes", ctypes.c_double)]
 
 
+class LayerStat(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 64), ("launches", ctypes.c_int64), ("ms", ctypes.c_double),
+                ("flop", ctypes.c_double), ("bytes", ctypes.c_double)]
+
+
 _P = ctypes.c_void_p
 _SIG = {
     "synerdiff_abi_version": (ctypes.c_int32, []),
@@ -60,6 +65,8 @@ _SIG = {
     "synerdiff_profile": (ctypes.c_int, [_P, ctypes.c_int32]),
     "synerdiff_profile_read": (ctypes.c_int, [_P, ctypes.POINTER(KernelStat), ctypes.c_int32,
                                               ctypes.POINTER(ctypes.c_int32), ctypes.c_int32]),
+    "synerdiff_profile_read_layers": (ctypes.c_int, [_P, ctypes.POINTER(LayerStat), ctypes.c_int32,
+                                                     ctypes.POINTER(ctypes.c_int32), ctypes.c_int32]),
     "synerdiff_op_conv": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, _P] + [ctypes.c_int32] * 7 +
                           [_P, _P, ctypes.c_int32, _P, ctypes.c_int32, _P, _P, _P, ctypes.c_int32, _P,
                            ctypes.c_int64, _P]),
@@ -67,7 +74,7 @@ _SIG = {
     "synerdiff_op_attention": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int64, ctypes.c_int64, _P,
                                               ctypes.c_int64, ctypes.c_int64, _P, ctypes.c_int64, ctypes.c_int64,
                                               ctypes.c_int32, _P, _P, ctypes.c_int64, ctypes.c_int64] +
-                               [ctypes.c_int32] * 5 + [ctypes.c_float, _P]),
+                               [ctypes.c_int32] * 5 + [ctypes.c_float, ctypes.c_int32, _P]),
     "synerdiff_op_groupnorm_scratch_floats": (ctypes.c_size_t, [ctypes.c_int32] * 3),
     "synerdiff_op_groupnorm_stats": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, _P] + [ctypes.c_int32] * 4 +
                                      [ctypes.c_float, _P, _P, _P, _P, _P, _P]),
@@ -230,6 +237,17 @@ class UNet:
         _check(lib().synerdiff_profile_read(self.h, arr, 16, ctypes.byref(n), int(reset)))
         return {arr[i].name.decode(): dict(launches=arr[i].launches, ms=arr[i].ms, flop=arr[i].flop,
                                            bytes=arr[i].bytes) for i in range(min(n.value, 16))}
+
+    def profile_read_layers(self, reset=True):
+        """{layer name: dict(launches, ms, flop, bytes)} since the last reset,
+        in first-launch order."""
+        n = ctypes.c_int32()
+        _check(lib().synerdiff_profile_read_layers(self.h, None, 0, ctypes.byref(n), 0))
+        cap = max(n.value, 1)
+        arr = (LayerStat * cap)()
+        _check(lib().synerdiff_profile_read_layers(self.h, arr, cap, ctypes.byref(n), int(reset)))
+        return {arr[i].name.decode(): dict(launches=arr[i].launches, ms=arr[i].ms, flop=arr[i].flop,
+                                           bytes=arr[i].bytes) for i in range(min(n.value, cap))}
 
     def close(self):
         if getattr(self, "h", None):

@@ -9,7 +9,25 @@
 // accumulator O^T = V^T P^T is a per-lane multiply.  The probabilities feed
 // the second MFMA straight from registers; the keys of each 16-key MFMA
 // slice are permuted to match the accumulator layout, and V^T is read from
-// LDS with the same permutation.  exp runs as exp2 on pre-scaled scores.
+// LDS with the same permutation.
+//
+// Softmax bookkeeping is kept off the vector ALU where the MFMAs can carry
+// it, since at SD head widths (d = 40) the exp and its companions, not the
+// products, bound the kernel:
+//  * Q arrives pre-scaled by scale * log2(e) (the projection GEMM's epilogue
+//    multiplies before its one rounding), so a score is already a base-2
+//    exponent and each probability is one exp2.  Unscaled Q is also
+//    accepted; then each score takes one fma more.
+//  * With pre-scaled Q, the running maximum m is subtracted inside the QK^T
+//    product when the head width leaves a spare padding column
+//    (d % 16 != 0): K carries a 1 in column d and Q carries -m there (m kept
+//    bf16-representable, so the product is exact).
+//  * The row sum of P comes out of the PV product when V^T has a spare
+//    padding row (d % 32 != 0): that row of V^T is 1 for every valid key.
+//  * m only moves when a tile's maximum exceeds it by more than 8 (so no
+//    probability exceeds 2^8); the rescale of the accumulators, the rare
+//    case after the first tile, is a wave-uniform branch.  The result is
+//    the same softmax: any m with no overflow gives the same quotient.
 // fp32: one thread per query, K/V tiles in LDS, fp32 online softmax.
 #include "device_common.h"
 #include "kernels.h"
@@ -17,61 +35,176 @@
 namespace sd {
 
 namespace fa {
-constexpr int KT = 64;  // keys per tile
+constexpr int KT = 64;        // keys per tile
+constexpr float TAU = 8.0f;   // lazy-rescale threshold (log2 units)
+}
+
+__device__ inline float bf16_rne(float x) { return (float)(bf16)x; }
+
+// v op v of lane l ^ 32: one lane-half swap instead of a trip through LDS.
+// (The builtin exists only for the device pass; the host pass never runs it.)
+__device__ inline float2 xor32_pair(float v) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return make_float2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+#else
+  return make_float2(v, v);
+#endif
+}
+__device__ inline float xor32_max(float v) {
+  const float2 p = xor32_pair(v);
+  return fmaxf(p.x, p.y);
+}
+__device__ inline float xor32_sum(float v) {
+  const float2 p = xor32_pair(v);
+  return p.x + p.y;
+}
+
+template <bool B>
+struct BC {
+  static constexpr bool value = B;
+};
+
+template <int V>
+struct IC {
+  static constexpr int value = V;
+};
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(IC<I>{});
+    static_for<I + 1, N>(f);
+  }
 }
 
 __device__ inline bf16x8 ld16(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
-// D16: head width rounded up to 16 (the QK^T reduction); DP: rounded up to
-// 32 (the PV output rows).  QG: groups of 32 queries per wave (the K and V
-// fragments read from LDS are reused across the groups).  VT: V is stored
-// transposed per image ([channel][token], written so by the projection
-// GEMM), so a V^T tile is staged with 16-byte loads and stores.
-template <int D16, int QG, bool VT, int NW>
-__global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a) {
+// Online-softmax step on one 64-key tile of S^T.  On entry s holds the raw
+// products: base-2 logits minus m when MF, base-2 logits when QS, plain
+// q.k otherwise.  Moves m where the tile exceeds it by more than TAU,
+// rescales the accumulators then, and leaves P = exp2(logit - m) in s.  SF:
+// the row sum comes out of the PV product, else it is added up here.
+template <int NJ, int ND, bool QS, bool MF, bool SF, bool TAIL>
+__device__ __forceinline__ void softmax_tile(f32x16 (&s)[2], f32x16 (&o)[ND], bf16x8 (&qf)[NJ], float& m_run,
+                                             float& l_run, bool first, int kvalid, int lh, int d, float sl2) {
   using namespace fa;
+  if constexpr (!QS) {
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kt][r] = fmaf(s[kt][r], sl2, -m_run);
+  } else if constexpr (!MF) {  // no spare column: subtract m here
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kt][r] -= m_run;
+  }
+  if constexpr (TAIL) {  // keys at or past kvalid; compared as immediates against one register
+    const int lim = kvalid - 4 * lh;
+    static_for<0, 32>([&](auto I) {
+      constexpr int kt = I.value / 16, r = I.value % 16;
+      if (kt * 32 + 8 * (r >> 2) + (r & 3) >= lim) s[kt][r] = -1e30f;
+    });
+  }
+  float mt = -1e30f;
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[kt][r]);
+  mt = xor32_max(mt);
+  const bool need = first || mt > TAU;
+  if (__any(need)) {
+    // move m to the (bf16-rounded) tile maximum where needed
+    float delta = 0.f;
+    if (need) {
+      const float mn = bf16_rne(m_run + mt);
+      delta = mn - m_run;
+      m_run = mn;
+    }
+    // (nothing has accumulated before the first tile; its delta may be any
+    // size, so alpha is not evaluated there)
+    const float alpha = first ? 0.f : __builtin_amdgcn_exp2f(-delta);
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kt][r] -= delta;
+    l_run *= alpha;
+#pragma unroll
+    for (int t = 0; t < ND; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+    if constexpr (MF) {
+      const bf16 nm = (bf16)(-m_run);
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (16 * j + 8 * lh + e == d) qf[j][e] = nm;
+    }
+  }
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s[kt][r] = __builtin_amdgcn_exp2f(s[kt][r]);
+  if constexpr (!SF) {
+    float ps = 0.f;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) ps += s[kt][r];
+    l_run += ps;
+  }
+}
+
+// D16: head width rounded up to 16 (the QK^T reduction); DP: rounded up to
+// 32 (the PV output rows).  QS: Q holds base-2 logit units (q * scale *
+// log2 e, written so by the projection GEMM).  MF (needs QS): d < D16, the
+// max rides in column d of the QK^T product.  SF: d < DP, the row sum rides
+// in row d of the PV product.  V is stored transposed per image
+// ([channel][token], as the projection GEMM writes it), so a V^T tile is
+// staged with 16-byte loads and stores.
+template <int D16, bool QS, bool MF, bool SF, int NW>
+__global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(AttnArgs a) {
+  using namespace fa;
+  static_assert(QS || !MF, "the max can ride in the product only with pre-scaled queries");
   constexpr int NJ = D16 / 16, DP = (D16 + 31) / 32 * 32, ND = DP / 32;
   constexpr int LDK = D16 + 8, LDV = KT + 8, NT = 64 * NW;
-  constexpr int KCH = KT * (D16 / 8), VCH = VT ? DP * (KT / 8) : KT * (DP / 8);  // 16-byte chunks per tile
-  constexpr int KPT = (KCH + NT - 1) / NT, VPT = (VCH + NT - 1) / NT;           // ... per thread
+  constexpr int KCH = KT * (D16 / 8), VCH = DP * (KT / 8);  // 16-byte chunks per tile
+  constexpr int KPT = (KCH + NT - 1) / NT, VPT = (VCH + NT - 1) / NT;  // ... per thread
   // Double-buffered K and V^T tiles; the next tile is fetched into registers
   // while the current one feeds the MFMAs.
   __shared__ __attribute__((aligned(16))) bf16 Ks[2][KT * LDK];
   __shared__ __attribute__((aligned(16))) bf16 Vt[2][DP * LDV];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int img = blockIdx.z, head = blockIdx.y;
-  const int qb = blockIdx.x * (32 * NW * QG) + wave * (32 * QG);
+  const int qb = blockIdx.x * (32 * NW) + wave * 32;
   const int kvimg = a.kv_index ? a.kv_index[img] : img;
   const int hd = head * a.d;
   const bf16* Q = reinterpret_cast<const bf16*>(a.q) + (long)img * a.q_img + hd;
   const bf16* K = reinterpret_cast<const bf16*>(a.k) + (long)kvimg * a.k_img + hd;
-  const bf16* V = reinterpret_cast<const bf16*>(a.v) + (long)kvimg * a.v_img + (VT ? (long)hd * a.v_ld : hd);
+  const bf16* V = reinterpret_cast<const bf16*>(a.v) + (long)kvimg * a.v_img + (long)hd * a.v_ld;
   const int lq = lane & 31, lh = lane >> 5;
+  const int d = a.d;
+  const float sl2 = a.scale * 1.4426950408889634f;  // used when !QS
 
-  // Q^T fragments (B operand): query qb + 32 g + lq, head dims 16 j + 8 lh + [0, 8).
-  bf16x8 qf[QG][NJ];
-#pragma unroll
-  for (int g = 0; g < QG; ++g) {
-    const int q = qb + 32 * g + lq;
+  // Q^T fragment (B operand): query qb + lq, head dims 16 j + 8 lh + [0, 8);
+  // column d (when MF) holds -m.
+  bf16x8 qf[NJ];
+  {
+    const int q = qb + lq;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
       const int dd = 16 * j + 8 * lh;
       const bf16x8 z = {};
-      qf[g][j] = (q < a.Nq && dd < a.d) ? ld16(Q + (long)q * a.q_ld + dd) : z;
+      qf[j] = (q < a.Nq && dd < d) ? ld16(Q + (long)q * a.q_ld + dd) : z;
     }
   }
-  f32x16 o[QG][ND];
-  float m_run[QG], l_run[QG];
+  f32x16 o[ND];
 #pragma unroll
-  for (int g = 0; g < QG; ++g) {
-    m_run[g] = -1e30f;
-    l_run[g] = 0.f;
+  for (int t = 0; t < ND; ++t)
 #pragma unroll
-    for (int t = 0; t < ND; ++t)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[g][t][r] = 0.f;
-  }
-  const float sl2 = a.scale * 1.4426950408889634f;
+    for (int r = 0; r < 16; ++r) o[t][r] = 0.f;
+  float m_run = 0.f, l_run = 0.f;
   const bool vvec = (a.v_ld & 7) == 0;
 
   bf16x8 rk[KPT], rv[VPT];
@@ -80,29 +213,34 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a) {
     for (int i = 0; i < KPT; ++i) {
       const int idx = tid + NT * i;
       const int key = idx / (D16 / 8), dc = (idx - key * (D16 / 8)) * 8;
-      const bf16x8 z = {};
-      rk[i] = (idx < KCH && k0 + key < a.Nk && dc < a.d) ? ld16(K + (long)(k0 + key) * a.k_ld + dc) : z;
+      bf16x8 v = {};
+      if (idx < KCH && k0 + key < a.Nk) {
+        if (dc < d)
+          v = ld16(K + (long)(k0 + key) * a.k_ld + dc);
+        else if (MF && dc == d)  // the column that subtracts m
+          v[0] = (bf16)1.0f;
+      }
+      rk[i] = v;
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
       const int idx = tid + NT * i;
+      const int dd = idx / (KT / 8), kc = (idx - dd * (KT / 8)) * 8;
+      const int k = k0 + kc;
       bf16x8 v = {};
-      if constexpr (VT) {
-        const int dd = idx / (KT / 8), kc = (idx - dd * (KT / 8)) * 8;
-        const int k = k0 + kc;
-        if (idx < VCH && dd < a.d && k < a.Nk) {
-          const bf16* src = V + (long)dd * a.v_ld + k;
-          if (vvec && k + 8 <= a.Nk) {
-            v = ld16(src);
-          } else {
+      if (idx < VCH && dd < d && k < a.Nk) {
+        const bf16* src = V + (long)dd * a.v_ld + k;
+        if (vvec && k + 8 <= a.Nk) {
+          v = ld16(src);
+        } else {
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-              if (k + e < a.Nk) v[e] = src[e];
-          }
+          for (int e = 0; e < 8; ++e)
+            if (k + e < a.Nk) v[e] = src[e];
         }
-      } else {
-        const int key = idx / (DP / 8), dc = (idx - key * (DP / 8)) * 8;
-        if (idx < VCH && k0 + key < a.Nk && dc < a.d) v = ld16(V + (long)(k0 + key) * a.v_ld + dc);
+      } else if (SF && idx < VCH && dd == d) {  // ones row: PV also sums P
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (k + e < a.Nk) v[e] = (bf16)1.0f;
       }
       rv[i] = v;
     }
@@ -117,22 +255,18 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
       const int idx = tid + NT * i;
-      if (idx >= VCH) continue;
-      if constexpr (VT) {
-        const int dd = idx / (KT / 8), kc = (idx - dd * (KT / 8)) * 8;
-        *reinterpret_cast<bf16x8*>(&Vt[b][dd * LDV + kc]) = rv[i];
-      } else {
-        const int key = idx / (DP / 8), dc = (idx - key * (DP / 8)) * 8;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) Vt[b][(dc + e) * LDV + key] = rv[i][e];
-      }
+      const int dd = idx / (KT / 8), kc = (idx - dd * (KT / 8)) * 8;
+      if (idx < VCH) *reinterpret_cast<bf16x8*>(&Vt[b][dd * LDV + kc]) = rv[i];
     }
   };
 
   fetch(0);
   stage(0);
   __syncthreads();
-  for (int k0 = 0, it = 0; k0 < a.Nk; k0 += KT, ++it) {
+  // One 64-key tile; the last tile, if partial, is a separate instance so
+  // the full tiles carry no masking code.
+  auto tile = [&](auto tl, int k0, int it) {
+    constexpr bool TAIL = decltype(tl)::value;
     const int b = it & 1;
     const bool more = k0 + KT < a.Nk;
     if (more) fetch(k0 + KT);
@@ -140,65 +274,27 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a) {
     const bf16* Vb = Vt[b];
 
     // S^T tiles: rows = keys kt*32 + 8(r/4) + 4 lh + r%4, col = query.
-    f32x16 s[QG][2];
+    f32x16 s[2];
 #pragma unroll
-    for (int g = 0; g < QG; ++g)
+    for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[g][kt][r] = 0.f;
+      for (int r = 0; r < 16; ++r) s[kt][r] = 0.f;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
         const bf16x8 kf = ld16(&Kb[(kt * 32 + lq) * LDK + 16 * j + 8 * lh]);
-#pragma unroll
-        for (int g = 0; g < QG; ++g) s[g][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[g][j], s[g][kt], 0, 0, 0);
+        s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[j], s[kt], 0, 0, 0);
       }
-    const bool tail = k0 + KT > a.Nk;
-#pragma unroll
-    for (int g = 0; g < QG; ++g) {
-      if (tail) {
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (k0 + kt * 32 + 8 * (r >> 2) + 4 * lh + (r & 3) >= a.Nk) s[g][kt][r] = -1e30f;
-      }
-      float mt = -1e30f;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[g][kt][r]);
-      mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * sl2;
-      const float m_new = fmaxf(m_run[g], mt);
-      const float alpha = __builtin_amdgcn_exp2f(m_run[g] - m_new);
-      m_run[g] = m_new;
-      float ps = 0.f;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[g][kt][r], sl2, -m_new));
-          s[g][kt][r] = p;
-          ps += p;
-        }
-      l_run[g] = l_run[g] * alpha + ps;
-#pragma unroll
-      for (int t = 0; t < ND; ++t)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[g][t][r] *= alpha;
-    }
+    softmax_tile<NJ, ND, QS, MF, SF, TAIL>(s, o, qf, m_run, l_run, it == 0, a.Nk - k0, lh, d, sl2);
 
     // O^T += V^T P^T over four 16-key slices.  Slot (lh, i) of slice u is
     // key 16u + 8(i/4) + 4 lh + i%4, i.e. register 8(u%2) + i of S^T tile u/2.
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      bf16x8 pf[QG];
+      bf16x8 pf;
 #pragma unroll
-      for (int g = 0; g < QG; ++g)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) pf[g][i] = (bf16)s[g][u >> 1][8 * (u & 1) + i];
+      for (int i = 0; i < 8; ++i) pf[i] = (bf16)s[u >> 1][8 * (u & 1) + i];
 #pragma unroll
       for (int t = 0; t < ND; ++t) {
         const bf16* vrow = &Vb[(t * 32 + lq) * LDV + 16 * u + 4 * lh];
@@ -207,35 +303,43 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a) {
         bf16x8 vf;
         vf[0] = lo[0]; vf[1] = lo[1]; vf[2] = lo[2]; vf[3] = lo[3];
         vf[4] = hi[0]; vf[5] = hi[1]; vf[6] = hi[2]; vf[7] = hi[3];
-#pragma unroll
-        for (int g = 0; g < QG; ++g) o[g][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[g], o[g][t], 0, 0, 0);
+        o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[t], 0, 0, 0);
       }
     }
     if (more) stage(b ^ 1);
     __syncthreads();
-  }
+  };
+  const int nfull = a.Nk / KT;
+  for (int it = 0; it < nfull; ++it) tile(BC<false>{}, it * KT, it);
+  if (nfull * KT < a.Nk) tile(BC<true>{}, nfull * KT, nfull);
 
   // O^T accumulator: lane holds head dims t*32 + 8(r/4) + 4 lh + [0, 4) of
   // its query; each run of 4 is one 8-byte store.
+  float l = l_run;
+  if constexpr (SF) {  // the ones row d of V^T accumulated the row sum into O^T row d
+    l = 0.f;
 #pragma unroll
-  for (int g = 0; g < QG; ++g) {
-    const float inv = 1.0f / (l_run[g] + __shfl_xor(l_run[g], 32, 64));
-    const int q = qb + 32 * g + lq;
-    if (q < a.Nq) {
-      bf16* O = reinterpret_cast<bf16*>(a.o) + (long)img * a.o_img + (long)q * a.o_ld + hd;
+    for (int t = 0; t < ND; ++t)
 #pragma unroll
-      for (int t = 0; t < ND; ++t)
+      for (int r = 0; r < 16; ++r)
+        if (32 * t + 8 * (r >> 2) + 4 * lh + (r & 3) == d) l = o[t][r];
+  }
+  const float inv = 1.0f / xor32_sum(l);
+  const int q = qb + lq;
+  if (q < a.Nq) {
+    bf16* O = reinterpret_cast<bf16*>(a.o) + (long)img * a.o_img + (long)q * a.o_ld + hd;
 #pragma unroll
-        for (int rg = 0; rg < 4; ++rg) {
-          const int dd = t * 32 + 8 * rg + 4 * lh;
-          if (dd < a.d) {
-            bf16x4 w;
+    for (int t = 0; t < ND; ++t)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) w[e] = (bf16)(o[g][t][4 * rg + e] * inv);
-            *reinterpret_cast<bf16x4*>(O + dd) = w;
-          }
+      for (int rg = 0; rg < 4; ++rg) {
+        const int dd = t * 32 + 8 * rg + 4 * lh;
+        if (dd < d) {
+          bf16x4 w;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) w[e] = (bf16)(o[t][4 * rg + e] * inv);
+          *reinterpret_cast<bf16x4*>(O + dd) = w;
         }
-    }
+      }
   }
 }
 
@@ -291,34 +395,59 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
   }
 }
 
-template <int D16, int QG>
+template <int D16, bool QS, bool MF, bool SF>
 static void launch_d(const AttnArgs& a, hipStream_t s) {
   constexpr int NW = 4;
-  dim3 grid((a.Nq + 32 * NW * QG - 1) / (32 * NW * QG), a.heads, a.imgs);
-  if (a.vt)
-    attn_bf16_kernel<D16, QG, true, NW><<<grid, 64 * NW, 0, s>>>(a);
-  else
-    attn_bf16_kernel<D16, QG, false, NW><<<grid, 64 * NW, 0, s>>>(a);
+  dim3 grid((a.Nq + 32 * NW - 1) / (32 * NW), a.heads, a.imgs);
+  attn_bf16_kernel<D16, QS, MF, SF, NW><<<grid, 64 * NW, 0, s>>>(a);
+}
+
+// Head widths d (multiples of 8) whose 16-rounding is D16: d = D16 - 8
+// carries the max (with pre-scaled queries) and the sum in the products;
+// d = D16 carries the sum when D16 is an odd multiple of 16.
+template <int D16>
+static void launch_w(const AttnArgs& a, hipStream_t s) {
+  constexpr bool odd = (D16 / 16) % 2 == 1;
+  if (a.q_log2) {
+    if (a.d < D16)
+      launch_d<D16, true, true, true>(a, s);
+    else
+      launch_d<D16, true, false, odd>(a, s);
+  } else {
+    if (a.d < D16)
+      launch_d<D16, false, false, true>(a, s);
+    else
+      launch_d<D16, false, false, odd>(a, s);
+  }
+}
+
+bool attention_width_ok(int d) {
+  if (d < 8 || d % 8) return false;
+  switch ((d + 15) / 16 * 16) {
+    case 16: case 32: case 48: case 64: case 80: case 96: case 128: case 160: case 192: case 256: return true;
+    default: return false;
+  }
 }
 
 hipError_t launch_attention(DType dt, const AttnArgs& a, hipStream_t s) {
   if (a.imgs <= 0 || a.Nq <= 0) return hipSuccess;
   if (dt == BF16) {
+    if (!attention_width_ok(a.d) || !a.vt) return hipErrorInvalidValue;
     switch ((a.d + 15) / 16 * 16) {
-      case 16: launch_d<16, 1>(a, s); break;
-      case 32: launch_d<32, 1>(a, s); break;
-      case 48: launch_d<48, 1>(a, s); break;
-      case 64: launch_d<64, 1>(a, s); break;
-      case 80: launch_d<80, 1>(a, s); break;
-      case 96: launch_d<96, 1>(a, s); break;
-      case 128: launch_d<128, 1>(a, s); break;
-      case 160: launch_d<160, 1>(a, s); break;
-      case 192: launch_d<192, 1>(a, s); break;
-      case 256: launch_d<256, 1>(a, s); break;
+      case 16: launch_w<16>(a, s); break;
+      case 32: launch_w<32>(a, s); break;
+      case 48: launch_w<48>(a, s); break;
+      case 64: launch_w<64>(a, s); break;
+      case 80: launch_w<80>(a, s); break;
+      case 96: launch_w<96>(a, s); break;
+      case 128: launch_w<128>(a, s); break;
+      case 160: launch_w<160>(a, s); break;
+      case 192: launch_w<192>(a, s); break;
+      case 256: launch_w<256>(a, s); break;
       default: return hipErrorInvalidValue;
     }
   } else {
-    if (a.vt) return hipErrorInvalidValue;
+    if (a.vt || a.q_log2) return hipErrorInvalidValue;
     dim3 grid((a.Nq + 63) / 64, a.heads, a.imgs);
     if (a.d <= 16)
       attn_f32_kernel<16><<<grid, 64, 0, s>>>(a);

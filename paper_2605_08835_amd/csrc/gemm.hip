@@ -96,6 +96,7 @@ __device__ inline void epilogue_store(const Epi& e, int row, int col, float v) {
   if (e.bias) v += e.bias[col];
   if (e.tbias) v += e.tbias[(long)(row / e.hw) * e.tb_ld + e.tb_off + col];
   if (e.resid) v += to_f(reinterpret_cast<const T*>(e.resid)[(long)row * e.ldr + col]);
+  if (col < e.qcols) v *= e.qscale;
   if (e.out_f32)
     reinterpret_cast<float*>(e.out)[(long)row * e.ldo + col] = v;
   else
@@ -130,6 +131,10 @@ __device__ inline void epilogue4(const Epi& e, int m, int n, float x[4]) {
     const bf16x4 r = *reinterpret_cast<const bf16x4*>(reinterpret_cast<const T*>(e.resid) + (long)m * e.ldr + n);
 #pragma unroll
     for (int i = 0; i < 4; ++i) x[i] += (float)r[i];
+  }
+  if (n < e.qcols) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) x[i] *= e.qscale;
   }
   store4<T>(e, m, n, x);
 }
@@ -830,7 +835,8 @@ hipError_t launch_gemm(DType dt, const GemmArgs& args, hipStream_t s) {
   if (a.ksplit > 1 && (dt != BF16 || !a.partial || a.epi.geglu || a.epi.vt_out || a.epi.out_f32 ||
                        a.N % 160 || loader_mode(a, DK) == 0))
     return hipErrorInvalidValue;
-  if (dt == BF16 && (a.N % 4 || a.epi.ldo % 4 || (a.epi.resid && a.epi.ldr % 4) || (a.epi.geglu && a.N % 32)))
+  if (dt == BF16 && (a.N % 4 || a.epi.ldo % 4 || (a.epi.resid && a.epi.ldr % 4) || (a.epi.geglu && a.N % 32) ||
+                     a.epi.qcols % 4))
     return hipErrorInvalidValue;
   if (dt != BF16 && (a.epi.geglu || a.epi.vt_out)) return hipErrorInvalidValue;
   if (a.epi.vt_out && (a.epi.vt_col0 % 8 || a.epi.resid || a.epi.bias || a.epi.tbias || a.epi.out_f32))

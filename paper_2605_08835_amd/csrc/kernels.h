@@ -46,6 +46,8 @@ struct Epi {
   int vt_col0, vt_hw;     //   vt_out[(m / vt_hw) * vt_img + (n - vt_col0) * vt_ld + m % vt_hw]
   int vt_ld;
   long vt_img;
+  int qcols;              // columns n < qcols are multiplied by qscale before rounding
+  float qscale;           //   (attention queries stored in base-2 logit units)
 };
 
 struct GemmArgs {
@@ -73,8 +75,12 @@ struct AttnArgs {
   void* o; long o_ld, o_img;
   int imgs, heads, d, Nq, Nk;
   float scale;
+  int q_log2;                        // 1: Q already holds q * scale * log2(e) (bf16 only)
 };
 hipError_t launch_attention(DType dt, const AttnArgs& a, hipStream_t s);
+// bf16 head widths the attention kernel is built for: d a multiple of 8
+// whose rounding up to 16 is 16..96, 128, 160, 192 or 256.
+bool attention_width_ok(int d);
 
 // GroupNorm statistics over up to two channel-concatenated NHWC sources;
 // writes per-(img, channel) scale = gamma*rstd and shift = beta - mean*scale.

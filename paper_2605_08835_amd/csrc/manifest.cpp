@@ -1,5 +1,7 @@
 #include "manifest.h"
 
+#include "kernels.h"
+
 namespace sd {
 
 namespace {
@@ -155,8 +157,7 @@ std::string check_config(const sd_unet_config& c) {
     const int d = c.heads ? ch / c.heads : c.head_dim;
     if (d % 8) return "head width must be a multiple of 8";
     if (c.dtype == SD_BF16) {
-      const int dp = (d + 31) / 32 * 32;
-      if (dp > 256 || dp == 224) return "bf16 head width must round up to 32..192 or 256";
+      if (!attention_width_ok(d)) return "bf16 head width must round up (to 16) to 16..96, 128, 160, 192 or 256";
     } else if (d > 64) {
       return "fp32 head width must be <= 64";
     }

@@ -92,13 +92,13 @@ sd_status synerdiff_op_attention(int32_t dtype, const void* q, int64_t q_ld, int
                                  int64_t k_ld, int64_t k_img, const void* v, int64_t v_ld, int64_t v_img,
                                  int32_t v_transposed, const int32_t* kv_index, void* o, int64_t o_ld,
                                  int64_t o_img, int32_t n, int32_t heads, int32_t d, int32_t nq, int32_t nk,
-                                 float scale, void* stream) {
+                                 float scale, int32_t q_log2, void* stream) {
   if (bad_dtype(dtype)) return op_fail(SD_ERR_INVALID_ARG, "bad dtype");
   if (!q || !k || !v || !o) return op_fail(SD_ERR_INVALID_ARG, "NULL argument");
   if (n < 0 || heads < 1 || d < 8 || d % 8 || nq < 0 || nk < 1) return op_fail(SD_ERR_INVALID_ARG, "bad shape");
-  const int dp = (d + 31) / 32 * 32;
-  if (dtype == SD_BF16 ? (dp > 256 || dp == 224) : d > 64) return op_fail(SD_ERR_UNSUPPORTED, "unsupported head width");
-  if (v_transposed && dtype != SD_BF16) return op_fail(SD_ERR_UNSUPPORTED, "transposed V is bf16 only");
+  if (dtype == SD_BF16 ? !attention_width_ok(d) : d > 64) return op_fail(SD_ERR_UNSUPPORTED, "unsupported head width");
+  if ((v_transposed != 0) != (dtype == SD_BF16)) return op_fail(SD_ERR_UNSUPPORTED, "V is transposed for bf16 and only for bf16");
+  if (q_log2 && dtype != SD_BF16) return op_fail(SD_ERR_UNSUPPORTED, "pre-scaled queries are bf16 only");
   if (n == 0 || nq == 0) return SD_OK;
   AttnArgs a;
   memset(&a, 0, sizeof(a));
@@ -107,7 +107,7 @@ sd_status synerdiff_op_attention(int32_t dtype, const void* q, int64_t q_ld, int
   a.v = v; a.v_ld = v_ld; a.v_img = v_img; a.vt = v_transposed ? 1 : 0;
   a.kv_index = kv_index;
   a.o = o; a.o_ld = o_ld; a.o_img = o_img;
-  a.imgs = n; a.heads = heads; a.d = d; a.Nq = nq; a.Nk = nk; a.scale = scale;
+  a.imgs = n; a.heads = heads; a.d = d; a.Nq = nq; a.Nk = nk; a.scale = scale; a.q_log2 = q_log2 ? 1 : 0;
   return op_hip(launch_attention((DType)dtype, a, (hipStream_t)stream), "attention");
 }
 

@@ -110,6 +110,7 @@ struct sd_unet {
   // profiling: one event after every launch; consecutive events bound it
   struct Rec {
     int kind;  // -1: start-of-step marker
+    int layer;  // index into layer_names
     double flops, bytes;
     hipEvent_t ev;
   };
@@ -120,6 +121,9 @@ struct sd_unet {
     long launches = 0;
     double ms = 0, flops = 0, bytes = 0;
   } tot[16];
+  std::map<std::string, int> layer_index;  // per-layer totals (name + shape)
+  std::vector<std::string> layer_names;
+  std::vector<Tot> ltot;
   // staging
   static constexpr int SLOTS = 8;
   uint8_t* pinned = nullptr;
@@ -310,14 +314,26 @@ static hipEvent_t take_event(sd_unet* h) {
   if (hipEventCreate(&e) != hipSuccess) return nullptr;
   return e;
 }
-static void prof_mark(sd_unet* h, int kind, double flops, double bytes, hipStream_t s) {
+static void prof_mark(sd_unet* h, int kind, const char* name, double flops, double bytes, hipStream_t s) {
   hipEvent_t e = take_event(h);
   if (!e) return;
   if (hipEventRecord(e, s) != hipSuccess) {
     h->pool.push_back(e);
     return;
   }
-  h->recs.push_back(sd_unet::Rec{kind, flops, bytes, e});
+  int layer = -1;
+  if (kind >= 0 && name) {
+    auto it = h->layer_index.find(name);
+    if (it == h->layer_index.end()) {
+      layer = (int)h->layer_names.size();
+      h->layer_index.emplace(name, layer);
+      h->layer_names.emplace_back(name);
+      h->ltot.emplace_back();
+    } else {
+      layer = it->second;
+    }
+  }
+  h->recs.push_back(sd_unet::Rec{kind, layer, flops, bytes, e});
 }
 static hipError_t prof_fold(sd_unet* h) {
   if (h->recs.empty()) return hipSuccess;
@@ -327,11 +343,13 @@ static hipError_t prof_fold(sd_unet* h) {
     if (r.kind < 0) continue;
     float ms = 0.f;
     err = hipEventElapsedTime(&ms, h->recs[i - 1].ev, r.ev);
-    auto& t = h->tot[r.kind];
-    t.launches++;
-    t.ms += ms;
-    t.flops += r.flops;
-    t.bytes += r.bytes;
+    for (sd_unet::Tot* t : {&h->tot[r.kind], r.layer >= 0 ? &h->ltot[r.layer] : nullptr}) {
+      if (!t) continue;
+      t->launches++;
+      t->ms += ms;
+      t->flops += r.flops;
+      t->bytes += r.bytes;
+    }
   }
   for (auto& r : h->recs) h->pool.push_back(r.ev);
   h->recs.clear();
@@ -362,7 +380,7 @@ struct Step {
       err = e;
       where = w;
     }
-    if (err == hipSuccess && h->prof) prof_mark(h, kind, flops, bytes, s);
+    if (err == hipSuccess && h->prof) prof_mark(h, kind, w, flops, bytes, s);
     return err == hipSuccess;
   }
   void* at(void* p, long elems) const { return p ? (uint8_t*)p + elems * h->esz : nullptr; }
@@ -450,7 +468,9 @@ struct Step {
     };
     double bytes = seg_bytes(s0, a.M) + (s1 ? seg_bytes(*s1, a.M) : 0.0) + (double)N * a.K * es +
                    (double)a.M * N * outb + (e.resid ? (double)a.M * N * es : 0.0);
-    ok(launch_gemm(h->dt, a, s), w, K_GEMM, 2.0 * a.M * N * K, bytes);
+    char key[64];
+    snprintf(key, sizeof(key), "%s %dx%dx%d", w, a.M, N, a.K);
+    ok(launch_gemm(h->dt, a, s), h->prof ? key : w, K_GEMM, 2.0 * a.M * N * K, bytes);
   }
   // ResBlock on [src0 | src1] (H x W) -> out (cout channels).
   void resblock(const ResW& r, const void* s0, int c0, const void* s1, int c1, int H, int W_, void* out,
@@ -494,8 +514,13 @@ struct Step {
       // bf16: Q|K row-major [T, 2C], V transposed per image [rows][C][hw]
       // (the layout the attention kernel stages with 16-byte loads).
       const bool vt = h->dt == BF16;
+      // bf16: queries leave the projection in base-2 logit units
+      // (q * log2(e) / sqrt(d), one rounding), as the attention kernel takes them
+      const float ql2 = 1.4426950408889634f / sqrtf((float)t.d);
       Epi eq = epi(q, vt ? 2 * C : 3 * C, nullptr);
       if (vt) {
+        eq.qcols = C;
+        eq.qscale = ql2;
         eq.vt_out = vbuf;
         eq.vt_col0 = 2 * C;
         eq.vt_hw = hw;
@@ -518,12 +543,22 @@ struct Step {
         a.o = x; a.o_ld = C; a.o_img = (long)hw * C;
         a.imgs = rows; a.heads = t.heads; a.d = t.d; a.Nq = hw; a.Nk = hw;
         a.scale = 1.0f / sqrtf((float)t.d);
-        ok(launch_attention(h->dt, a, s), "self-attention", K_ATTN, 4.0 * rows * hw * (double)hw * C,
+        a.q_log2 = vt ? 1 : 0;
+        char key[64];
+        snprintf(key, sizeof(key), "self-attention %dx%d d%d", hw, hw, t.d);
+        ok(launch_attention(h->dt, a, s), key, K_ATTN, 4.0 * rows * hw * (double)hw * C,
            4.0 * T * C * h->esz);
       }
       gemm(lin(x, C, T), nullptr, W(b.o1w), C, epi(z, C, Wf(b.o1b), z, C), "attn1.out", T);
       if (!dry && !err) ok(launch_layernorm(h->dt, z, x, T, C, Wf(b.ln2g), Wf(b.ln2b), 1e-5f, s), "ln2", K_LN, 8.0 * T * C, 2.0 * T * C * h->esz);
-      gemm(lin(x, C, T), nullptr, W(b.q2), C, epi(q, C, nullptr), "attn2.q", T);
+      {
+        Epi e2 = epi(q, C, nullptr);
+        if (h->dt == BF16) {
+          e2.qcols = C;
+          e2.qscale = 1.4426950408889634f / sqrtf((float)t.d);
+        }
+        gemm(lin(x, C, T), nullptr, W(b.q2), C, e2, "attn2.q", T);
+      }
       {
         const bool vt = h->dt == BF16;
         Epi ek = epi(ckv, vt ? C : 2 * C, nullptr);
@@ -550,7 +585,10 @@ struct Step {
           a.o = x; a.o_ld = C; a.o_img = (long)hw * C;
           a.imgs = rows; a.heads = t.heads; a.d = t.d; a.Nq = hw; a.Nk = L;
           a.scale = 1.0f / sqrtf((float)t.d);
-          ok(launch_attention(h->dt, a, s), "cross-attention", K_ATTN, 4.0 * rows * hw * (double)L * C,
+          a.q_log2 = vt ? 1 : 0;
+          char key[64];
+          snprintf(key, sizeof(key), "cross-attention %dx%d d%d", hw, L, t.d);
+          ok(launch_attention(h->dt, a, s), key, K_ATTN, 4.0 * rows * hw * (double)L * C,
              (2.0 * T * C + 2.0 * (n_req + 1) * L * C) * h->esz);
         }
       }
@@ -587,7 +625,7 @@ struct Step {
     const float* req_coef = (const float*)(scal + 4 * (9 * R));
     const float* time_ids = (const float*)(scal + 4 * (12 * R));
 
-    if (!dry && h->prof) prof_mark(h, -1, 0, 0, s);
+    if (!dry && h->prof) prof_mark(h, -1, nullptr, 0, 0, s);
     // contexts: [cond_0 .. cond_{n-1}, uncond]
     void* ctx = buf(R_CTX, (size_t)(n_req + 1) * L * D * h->esz);
     if (!dry && !err) {
@@ -1097,6 +1135,30 @@ sd_status synerdiff_profile_read(sd_unet* h, sd_kernel_stat* out, int32_t cap, i
   *n_out = n;
   if (reset)
     for (auto& t : h->tot) t = sd_unet::Tot();
+  return SD_OK;
+}
+
+sd_status synerdiff_profile_read_layers(sd_unet* h, sd_layer_stat* out, int32_t cap, int32_t* n_out,
+                                        int32_t reset) {
+  if (!h || !n_out || (cap > 0 && !out)) return fail(SD_ERR_INVALID_ARG, "NULL argument");
+  if (prof_fold(h) != hipSuccess) return fail(SD_ERR_HIP, "profiling event query failed");
+  int n = 0;
+  for (size_t i = 0; i < h->ltot.size(); ++i) {
+    if (!h->ltot[i].launches) continue;
+    if (n < cap) {
+      sd_layer_stat& o = out[n];
+      memset(&o, 0, sizeof(o));
+      strncpy(o.name, h->layer_names[i].c_str(), sizeof(o.name) - 1);
+      o.launches = h->ltot[i].launches;
+      o.ms = h->ltot[i].ms;
+      o.flop = h->ltot[i].flops;
+      o.bytes = h->ltot[i].bytes;
+    }
+    ++n;
+  }
+  *n_out = n;
+  if (reset)
+    for (auto& t : h->ltot) t = sd_unet::Tot();
   return SD_OK;
 }
 

@@ -33,10 +33,10 @@ def conv(x0, w_packed, cout, ks=3, stride=1, up=0, x1=None, scale=None, shift=No
 
 
 def attention(q, k, v, o, n, heads, d, n_q, n_k, q_ld, q_img, k_ld, k_img, v_ld, v_img, o_ld, o_img, scale,
-              kv_index=None, v_transposed=False):
+              kv_index=None, v_transposed=False, q_log2=False):
     _check(lib().synerdiff_op_attention(_dt(q), _ptr(q), q_ld, q_img, _ptr(k), k_ld, k_img, _ptr(v), v_ld, v_img,
                                         int(v_transposed), _ptr(kv_index), _ptr(o), o_ld, o_img, n, heads, d, n_q,
-                                        n_k, float(scale), _s()))
+                                        n_k, float(scale), int(q_log2), _s()))
     return o
 
 

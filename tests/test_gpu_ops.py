@@ -99,18 +99,23 @@ def test_conv(ops, dt, case):
         assert err <= TOL[dt], (i, err)
 
 
-@pytest.mark.parametrize("vt", [False, True])
+@pytest.mark.parametrize("qmode", ["plain", "log2"])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("heads,d,nq,nk,scale,cross", [
     (2, 8, 70, 70, 1.0, False), (2, 16, 33, 8, 1.0, True), (4, 32, 200, 200, 1.0, False),
     (8, 40, 300, 300, 1.0, False), (8, 40, 129, 77, 1.0, True), (2, 64, 256, 256, 30.0, False),
     (8, 80, 160, 160, 1.0, False), (8, 160, 64, 64, 1.0, False), (8, 160, 90, 77, 1.0, True),
-    (2, 40, 36, 36, 1.0, False),
+    (2, 40, 36, 36, 1.0, False), (2, 24, 130, 130, 1.0, False), (1, 48, 64, 200, 30.0, True),
+    (4, 56, 65, 129, 1.0, False), (2, 72, 100, 100, 1.0, False), (2, 128, 70, 70, 1.0, False),
 ])
-def test_attention(ops, dt, vt, heads, d, nq, nk, scale, cross):
-    if dt == "f32" and (d > 64 or vt):
-        pytest.skip("fp32 attention covers head widths <= 64 with row-major V")
-    log(f"attention {dt} vt={vt} heads={heads} d={d} nq={nq} nk={nk} x{scale} cross={cross}")
+def test_attention(ops, dt, qmode, heads, d, nq, nk, scale, cross):
+    """bf16 takes V transposed (channel-major, padded token stride, as the
+    step stores it); "log2" passes Q pre-multiplied by scale * log2(e) and
+    rounded once, as the projection epilogue writes it, and the reference
+    uses exactly that Q (divided back in float64)."""
+    if dt == "f32" and (d > 64 or qmode == "log2"):
+        pytest.skip("fp32 attention covers head widths <= 64 with row-major V and plain Q")
+    log(f"attention {dt} {qmode} heads={heads} d={d} nq={nq} nk={nk} x{scale} cross={cross}")
     rng = np.random.default_rng(d * 1000 + nq)
     C = heads * d
     n = 3
@@ -120,7 +125,13 @@ def test_attention(ops, dt, vt, heads, d, nq, nk, scale, cross):
     v = _vals(rng, (nkv, nk, C), dt)
     idx = np.array([1, 0, 1], np.int32) if cross else None
     o = torch.empty(n, nq, C, device="cuda", dtype=_tdt(dt))
-    if vt:  # channel-major V with a padded token stride, as the step stores it
+    sm = 1.0 / math.sqrt(d)
+    qref = q.astype(np.float64)
+    if qmode == "log2":
+        sl2 = sm * math.log2(math.e)
+        q = bf16_round((q.astype(np.float64) * sl2).astype(np.float32))
+        qref = q.astype(np.float64) / sl2
+    if dt == "bf16":  # channel-major V with a padded token stride
         ld = (nk + 7) // 8 * 8
         vdev = torch.zeros(nkv, C, ld, device="cuda", dtype=_tdt(dt))
         vdev[:, :, :nk] = _dev(v, dt).transpose(1, 2)
@@ -128,12 +139,13 @@ def test_attention(ops, dt, vt, heads, d, nq, nk, scale, cross):
     else:
         vdev, v_ld, v_img = _dev(v, dt), C, nk * C
     ops.attention(_dev(q, dt), _dev(k, dt), vdev, o, n, heads, d, nq, nk, C, nq * C, C, nk * C, v_ld, v_img,
-                  C, nq * C, 1.0 / math.sqrt(d), kv_index=_dev(idx) if cross else None, v_transposed=vt)
+                  C, nq * C, sm, kv_index=_dev(idx) if cross else None, v_transposed=dt == "bf16",
+                  q_log2=qmode == "log2")
     torch.cuda.synchronize()
     got = o.float().cpu().numpy()
     for i in range(n):
         j = idx[i] if cross else i
-        ref = O.attention(q[i].astype(np.float64), k[j].astype(np.float64), v[j].astype(np.float64), heads)
+        ref = O.attention(qref[i], k[j].astype(np.float64), v[j].astype(np.float64), heads)
         err = rel_l2(got[i], ref)
         # fp32 scores carry a relative rounding error ~2^-24 |s|; with logits
         # scaled x30 (|s| ~ 1e3) that reaches the output as ~1e-4.
