@@ -153,18 +153,27 @@ hipError_t launch_linear_smallm(DType wdt, const float* in, int M, int K, const 
 }
 
 // --------------------------------------------------------- GroupNorm stats
-// Pass 1: per (img, pixel chunk) fp32 sums and sums of squares per channel.
-// Threads (cv, pp): channel vector cv (8 channels, one 16-byte load) of
-// pixels p0 + pp, p0 + pp + PP, ...; partial results reduced over pp in LDS.
-static inline int gn_splits(int hw) {
-  int s = (hw + 63) / 64;
+// Pixel rows per block of the partial pass: enough threads to stream a
+// block's pixels with several 16-byte loads in flight each.
+static inline int gn_pp(int cin) {
+  const int cv = cin / 8;
+  return cv >= 512 ? 1 : 512 / cv;
+}
+// Splits of an image's pixels (about 8 pixels per thread, at most 64).
+static inline int gn_splits(int hw, int cin) {
+  const int s = hw / (gn_pp(cin) * 8);
   return s < 1 ? 1 : (s > 64 ? 64 : s);
 }
 
 size_t groupnorm_partial_floats(int imgs, int hw, int cin) {
-  return (size_t)imgs * gn_splits(hw) * cin * 2;
+  return (size_t)imgs * gn_splits(hw, cin) * cin * 2;
 }
 
+// Pass 1: per (image, split, channel) sum and sum of squares (fp32 over at
+// most a few hundred pixels; the finalize pass adds the splits in fp64).
+// Thread (pp, cv) reads channels 8 cv .. 8 cv + 7 (one 16-byte load) of
+// pixels pp, pp + PP, ..., four at a time so their loads overlap; the
+// partial results are reduced over pp in LDS.
 template <typename T>
 __global__ void gn_partial_kernel(const T* src0, int c0, const T* src1, int c1, int hw, int nsplit,
                                   int PP, float* partial) {
@@ -175,20 +184,29 @@ __global__ void gn_partial_kernel(const T* src0, int c0, const T* src1, int c1, 
   const int p0 = split * chunk, p1 = min(hw, p0 + chunk);
   const int cv = threadIdx.x % CV, pp = threadIdx.x / CV;
   const int c = cv * 8;
+  const T* base = c < c0 ? src0 + c : src1 + (c - c0);
+  const int ld = c < c0 ? c0 : c1;
   float s[8] = {}, q[8] = {};
   if (pp < PP) {
-    for (int p = p0 + pp; p < p1; p += PP) {
-      float v[8];
-      const long pix = (long)img * hw + p;
-      if (c < c0)
-        load8f(src0 + pix * c0 + c, v);
-      else
-        load8f(src1 + pix * c1 + (c - c0), v);
+    for (int p = p0 + pp; p < p1; p += 4 * PP) {
+      float v[4][8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        s[i] += v[i];
-        q[i] = fmaf(v[i], v[i], q[i]);
+      for (int u = 0; u < 4; ++u) {
+        const int pu = p + u * PP;
+        if (pu < p1) {
+          load8f(base + ((long)img * hw + pu) * ld, v[u]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) v[u][i] = 0.f;
+        }
       }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          s[i] += v[u][i];
+          q[i] = fmaf(v[u][i], v[u][i], q[i]);
+        }
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -209,33 +227,33 @@ __global__ void gn_partial_kernel(const T* src0, int c0, const T* src1, int c1, 
   }
 }
 
-// Pass 2: one wave per group merges the partials in fp64 and writes the
-// per-(img, channel) affine scale = gamma * rstd, shift = beta - mean * scale.
+// Pass 2: per (image, group) mean and rstd in fp64 -> the per-channel affine.
+// One wave per (group, image); the loads of a lane's partials are
+// independent, so the loop is unrolled to keep them in flight together.
 __global__ void gn_finalize_kernel(const float* partial, int cin, int nsplit, int hw, int groups,
                                    float eps, const float* gamma, const float* beta, float* scale,
                                    float* shift) {
-  const int img = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int cpg = cin / groups;
-  for (int g = wave; g < groups; g += blockDim.x / 64) {
-    double s = 0.0, q = 0.0;
-    for (int idx = lane; idx < nsplit * cpg; idx += 64) {
-      const int sp = idx / cpg, ch = g * cpg + (idx - sp * cpg);
-      const float* p = partial + (((long)img * nsplit + sp) * cin + ch) * 2;
-      s += p[0];
-      q += p[1];
-    }
-    s = wave_sum_d(s);
-    q = wave_sum_d(q);
-    const double n = (double)cpg * hw;
-    const double mean = s / n;
-    double var = q / n - mean * mean;
-    if (var < 0.0) var = 0.0;
-    const float rstd = (float)(1.0 / sqrt(var + (double)eps));
-    for (int ch = g * cpg + lane; ch < (g + 1) * cpg; ch += 64) {
-      const float sc = gamma[ch] * rstd;
-      scale[(long)img * cin + ch] = sc;
-      shift[(long)img * cin + ch] = beta[ch] - (float)mean * sc;
-    }
+  const int g = blockIdx.x, img = blockIdx.y, lane = threadIdx.x;
+  const int cpg = cin / groups, n = nsplit * cpg;
+  double s = 0.0, q = 0.0;
+#pragma unroll 8
+  for (int idx = lane; idx < n; idx += 64) {
+    const int sp = idx / cpg, ch = g * cpg + (idx - sp * cpg);
+    const float2 v = *reinterpret_cast<const float2*>(partial + (((long)img * nsplit + sp) * cin + ch) * 2);
+    s += v.x;
+    q += v.y;
+  }
+  s = wave_sum_d(s);
+  q = wave_sum_d(q);
+  const double cnt = (double)cpg * hw;
+  const double mean = s / cnt;
+  double var = q / cnt - mean * mean;
+  if (var < 0.0) var = 0.0;
+  const float rstd = (float)(1.0 / sqrt(var + (double)eps));
+  for (int ch = g * cpg + lane; ch < (g + 1) * cpg; ch += 64) {
+    const float sc = gamma[ch] * rstd;
+    scale[(long)img * cin + ch] = sc;
+    shift[(long)img * cin + ch] = beta[ch] - (float)mean * sc;
   }
 }
 
@@ -245,8 +263,8 @@ hipError_t launch_groupnorm_stats(DType dt, const void* src0, int c0, const void
                                   hipStream_t s) {
   if (imgs == 0) return hipSuccess;
   const int cin = c0 + c1, CV = cin / 8;
-  const int PP = CV >= 256 ? 1 : 256 / CV;
-  const int nsplit = gn_splits(hw);
+  const int PP = gn_pp(cin);
+  const int nsplit = gn_splits(hw, cin);
   const int threads = CV * PP;
   const size_t lds = (size_t)PP * cin * 2 * sizeof(float);
   if (threads > 1024 || lds > 64 * 1024) return hipErrorInvalidValue;
@@ -259,8 +277,8 @@ hipError_t launch_groupnorm_stats(DType dt, const void* src0, int c0, const void
                                                         c1, hw, nsplit, PP, partial);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  gn_finalize_kernel<<<imgs, 256, 0, s>>>(partial, cin, nsplit, hw, groups, eps, gamma, beta, scale,
-                                          shift);
+  gn_finalize_kernel<<<dim3(groups, imgs), 64, 0, s>>>(partial, cin, nsplit, hw, groups, eps, gamma, beta,
+                                                       scale, shift);
   return hipGetLastError();
 }
 

@@ -62,6 +62,15 @@ CONV_CASES = [
     (2, 4, 4, 640, 640, 320, 3, 1, 0, False),
     (3, 4, 4, 1280, 0, 160, 3, 2, 0, False),
     (2, 2, 2, 640, 0, 320, 3, 1, 1, False),
+    # enough rows for the 256x320 eight-wave tiles (ragged, concat, stride 2, upsampling)
+    (65, 32, 32, 64, 0, 320, 3, 1, 0, False),
+    (32, 32, 32, 64, 64, 640, 3, 1, 0, False),
+    (64, 64, 64, 32, 0, 320, 3, 2, 0, False),
+    (64, 16, 16, 64, 0, 320, 3, 1, 1, False),
+    (67, 32, 32, 320, 0, 320, 1, 1, 0, False),
+    # more blocks than fit on the chip at once (ragged, split K)
+    (130, 32, 32, 64, 0, 160, 3, 1, 0, False),
+    (150, 8, 8, 640, 0, 320, 3, 1, 0, False),
 ]
 
 
@@ -216,3 +225,14 @@ def test_conv_split_k_rows_independent(ops, n):
     err = rel_l2(part, nosplit)
     log(f"split-K n={n}: rel L2 vs one pass {err:.2e}")
     assert err < 1e-2
+
+
+def test_conv_large_grid_rows_independent(ops):
+    """An image gets the same bits in a grid of 560 tiles as alone."""
+    rng = np.random.default_rng(22)
+    x = _vals(rng, (140, 32, 32, 64), "bf16")
+    w = _vals(rng, (160, 64, 3, 3), "bf16", 0.05)
+    wp = _dev(_pack(w), "bf16")
+    full = ops.conv(_dev(x, "bf16"), wp, 160)[:3].float().cpu().numpy()
+    part = ops.conv(_dev(x[:3], "bf16"), wp, 160).float().cpu().numpy()
+    assert np.array_equal(full, part)
