@@ -30,8 +30,103 @@ PEAK_HBM = 8.0e12
 FLOP_PER_ROW = 803.27e9  # algorithmic FLOPs of one SD-1.5 UNet evaluation at 64x64
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_sd15_48rows_traffic.md")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2605_08835_amd", "csrc", "gemm.hip")
+
+
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_class(name):
+    """Kernel class of a device kernel name (the classes of the step's profile)."""
+    for key, cls in (("gemm_bf16", "gemm"), ("gemm_f32", "gemm"), ("splitk_reduce", "gemm"),
+                     ("attn_", "attention"), ("gn_apply", "groupnorm apply"), ("gn_", "groupnorm"),
+                     ("layernorm", "layernorm"), ("geglu", "geglu"), ("linear_smallm", "time_mlp"),
+                     ("time_inputs", "time_mlp"), ("pack_latents", "pack"), ("cfg_ddim", "cfg_ddim")):
+        if key in name:
+            return cls
+    return None
+
+
+def source_digest(path):
+    import hashlib
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def stored_traffic():
+    """HBM bytes per GEMM launch from the committed counter summary, if it was
+    taken on the GEMM source as it is now (else None)."""
+    import re
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None
+    mb = re.search(r"traffic_bytes_per_launch\s*\|\s*([0-9.eE+]+)", text)
+    md = re.search(r"gemm\.hip sha256\s*\|\s*([0-9a-f]{64})", text)
+    if not mb or not md or md.group(1) != source_digest(GEMM_SOURCE):
+        return None
+    return float(mb.group(1))
+
+
+def summarize(stats_dir=None, fetch_dir=None, write_dir=None, copy_bytes=None):
+    """Markdown summary of rocprofv3 output: per-kernel statistics (from a
+    --kernel-trace --stats run) and, from two --pmc runs, the HBM bytes per
+    GEMM launch calibrated on the plain copy kernel of copy_bytes each way."""
+    import csv
+    import glob
+    out = []
+    if stats_dir:
+        f = glob.glob(os.path.join(stats_dir, "**", "*kernel_stats.csv"), recursive=True)[0]
+        rows = list(csv.DictReader(open(f)))
+        out.append("| kernel | class | calls | total ms | avg us |")
+        out.append("|---|---|---|---|---|")
+        tot = {}
+        for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+            cls = kernel_class(r["Name"])
+            calls, ns = int(r["Calls"]), float(r["TotalDurationNs"])
+            out.append(f"| `{r['Name'][:90]}` | {cls} | {calls} | {ns / 1e6:.3f} | {ns / calls / 1e3:.1f} |")
+            if cls:
+                t = tot.setdefault(cls, [0, 0.0])
+                t[0] += 0 if ("splitk_reduce" in r["Name"] or "gn_finalize" in r["Name"]) else calls
+                t[1] += ns
+        out.append("")
+        out.append("| class | launches | total ms | avg us per launch |")
+        out.append("|---|---|---|---|")
+        for cls, (calls, ns) in sorted(tot.items(), key=lambda kv: -kv[1][1]):
+            out.append(f"| {cls} | {calls} | {ns / 1e6:.3f} | {ns / max(calls, 1) / 1e3:.1f} |")
+    if fetch_dir and write_dir:
+        def per_dispatch(d, counter):
+            f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+            vals = {}
+            for r in csv.DictReader(open(f)):
+                if r["Counter_Name"] == counter:
+                    vals[r["Dispatch_Id"]] = (r["Kernel_Name"], vals.get(r["Dispatch_Id"], ("", 0.0))[1]
+                                              + float(r["Counter_Value"]))
+            return list(vals.values())
+        fetch, write = per_dispatch(fetch_dir, "FETCH_SIZE"), per_dispatch(write_dir, "WRITE_SIZE")
+        cal_f = max(v for n, v in fetch if "elementwise" in n)
+        cal_w = max(v for n, v in write if "elementwise" in n)
+        kf, kw = copy_bytes / (cal_f * 1024), copy_bytes / (cal_w * 1024)
+        g_f = sum(v for n, v in fetch if kernel_class(n) == "gemm")
+        g_w = sum(v for n, v in write if kernel_class(n) == "gemm")
+        launches = sum(1 for n, _ in fetch if kernel_class(n) == "gemm" and "splitk_reduce" not in n)
+        per = (g_f * 1024 * kf + g_w * 1024 * kw) / launches
+        out.append("")
+        out.append("| quantity | value |")
+        out.append("|---|---|")
+        out.append(f"| copy kernel bytes each way | {copy_bytes} |")
+        out.append(f"| FETCH_SIZE of the copy (KiB) | {cal_f:.0f} |")
+        out.append(f"| WRITE_SIZE of the copy (KiB) | {cal_w:.0f} |")
+        out.append(f"| fetch scale | {kf:.4f} |")
+        out.append(f"| write scale | {kw:.4f} |")
+        out.append(f"| GEMM launches | {launches} |")
+        out.append(f"| GEMM fetch bytes (scaled) | {g_f * 1024 * kf:.4e} |")
+        out.append(f"| GEMM write bytes (scaled) | {g_w * 1024 * kw:.4e} |")
+        out.append(f"| traffic_bytes_per_launch | {per:.4e} |")
+        out.append(f"| gemm.hip sha256 | {source_digest(GEMM_SOURCE)} |")
+    return "\n".join(out)
 
 
 def cpu_baseline(unet, weights, req, budget_s=25.0):
@@ -69,7 +164,16 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layers", default=None, help="write a per-layer device-time table to this file")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="run a plain copy kernel of MIB MiB each way first (counter calibration)")
+    ap.add_argument("--summarize", nargs="*", metavar="DIR",
+                    help="print a markdown summary of rocprofv3 output: STATS_DIR [FETCH_DIR WRITE_DIR] "
+                         "(the copy size comes from --calibrate-copy)")
     args = ap.parse_args()
+    if args.summarize is not None:
+        d = args.summarize + [None] * 3
+        print(summarize(d[0], d[1], d[2], args.calibrate_copy * 2**20))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the step shards by request with no collective, "
               f"and this build runs on a single MI355X (got --gpus {args.gpus}).", file=sys.stderr)
@@ -98,6 +202,13 @@ def main():
     coef = m.coefficients(req["schedule"], req["timesteps"], req["t_prev"])
     out = torch.empty_like(lat)
     stream = torch.cuda.current_stream(dev)
+    if args.calibrate_copy:
+        n = args.calibrate_copy * 2**20 // 4
+        src, dst = torch.ones(n, device=dev), torch.empty(n, device=dev)
+        for _ in range(3):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     def step():
         m.step(lat, req["timesteps"], req["cfg_on"], req["guidance"], ctx, unc, coef, out=out, stream=stream)
@@ -147,7 +258,7 @@ def main():
     achieved = flop_per_launch / avg_s / 1e12
     roof = {"kernel": "gemm_bf16_kernel (implicit-GEMM conv / linear, MFMA 32x32x16 bf16)",
             "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
-            "frac": round(achieved * 1e12 / PEAK_BF16, 4), "traffic": None,
+            "frac": round(achieved * 1e12 / PEAK_BF16, 4), "traffic": stored_traffic(),
             "flop_per_launch": flop_per_launch, "launches_per_step": g_launches,
             "avg_launch_us": round(avg_s * 1e6, 2)}
 
