@@ -437,7 +437,15 @@ __global__ __launch_bounds__(256, MINB) void gemm_bf16_kernel(GemmArgs a) {
 // c ^ ((r >> 2) & 3), which keeps the fragment reads of 8 consecutive rows
 // on distinct banks.  Lane l of a load writes (row 16 i + l / 4, slot l % 4)
 // and therefore fetches chunk (l % 4) ^ ((row >> 2) & 3) from global memory.
-constexpr int DK = 32;  // K depth per stage
+constexpr int DKS = 32;  // K depth per stage (the split-K and loader-mode granule)
+
+// Slot swizzle of a tile row's 16-byte chunks: the fragment reads of rows
+// r..r+15 at one logical chunk land on distinct 16-byte bank groups (4
+// chunks per row: 64-byte rows; 8 chunks: 128-byte rows).
+template <int CPR>
+__device__ __forceinline__ int swz(int r) {
+  return CPR == 4 ? (r >> 2) & 3 : (r >> 1) & 7;
+}
 
 // One 16-byte-per-lane direct-to-LDS load (64 lanes -> 1 KB at `lds`).
 // The builtin exists only for the device pass; the host pass of this file
@@ -455,14 +463,17 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((WAITN & 15) | (7 << 4) | (15 << 8) | ((WAITN >> 4) << 14));
 }
 
-template <int BM, int BN, int WM, int WN, int MODE, int DNS, int MINB>
-__global__ __launch_bounds__(256, MINB) void gemm_bf16_dma_kernel(GemmArgs a) {
+template <int BM, int BN, int WM, int WN, int MODE, int DNS, int MINB, int DK>
+__global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmArgs a) {
+  constexpr int NWV = WM * WN;                          // waves per block
   constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
-  constexpr int AI = BM / 16, BI = BN / 16;             // 1 KB loads per tile
-  constexpr int AW = AI / 4, BW = (BI + 3) / 4;         // ... per wave (B: some waves one fewer)
-  constexpr int LPT_MIN = AW + BI / 4;                  // loads per tile of the lightest wave
+  constexpr int CPR = DK / 8, RPL = 64 / CPR;           // 16-byte chunks per row, rows per load
+  constexpr int AI = BM / RPL, BI = BN / RPL;           // 1 KB loads per tile
+  constexpr int AW = AI / NWV, BW = (BI + NWV - 1) / NWV;  // ... per wave (B: some waves one fewer)
+  constexpr int LPT_MIN = AW + BI / NWV;                // loads per tile of the lightest wave
   static_assert(DNS >= 2 && DNS <= 4, "pipeline depth");
-  static_assert(AI % 4 == 0, "A tile must split evenly over 4 waves");
+  static_assert(DK == 32 || DK == 64, "stage depth");
+  static_assert(AI % NWV == 0, "A tile must split evenly over the waves");
   __shared__ __attribute__((aligned(1024))) bf16 As[DNS][BM * DK];
   __shared__ __attribute__((aligned(1024))) bf16 Bs[DNS][BN * DK];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -478,15 +489,15 @@ __global__ __launch_bounds__(256, MINB) void gemm_bf16_dma_kernel(GemmArgs a) {
   const int m0 = tm * BM, n0 = tn * BN;
 
   // Rows and chunks this lane fetches: A load j of this wave is tile load
-  // i = wave * AW + j (rows 16 i ..); B load j is i = wave + 4 j.
-  const int lrow = lane >> 2, lslot = lane & 3;
+  // i = wave * AW + j (rows RPL i ..); B load j is i = wave + NWV j.
+  const int lrow = lane / CPR, lslot = lane % CPR;
   const int Ho = a.seg[0].Ho, Wo = a.seg[0].Wo, hwo = Ho * Wo;
   int ra0[AW], ra1[AW], achunk[AW];
 #pragma unroll
   for (int j = 0; j < AW; ++j) {
-    const int r = 16 * (wave * AW + j) + lrow;
+    const int r = RPL * (wave * AW + j) + lrow;
     const int m = m0 + r;
-    achunk[j] = lslot ^ ((r >> 2) & 3);
+    achunk[j] = lslot ^ swz<CPR>(r);
     if constexpr (MODE == 1) {
       const int p = m % hwo, oy = p / Wo, ox = p - oy * Wo;
       int mk = 0;
@@ -507,10 +518,10 @@ __global__ __launch_bounds__(256, MINB) void gemm_bf16_dma_kernel(GemmArgs a) {
   int boff[BW];
 #pragma unroll
   for (int j = 0; j < BW; ++j) {
-    const int i = wave + 4 * j;
-    const int r = 16 * i + lrow;
+    const int i = wave + NWV * j;
+    const int r = RPL * i + lrow;
     const int n = n0 + r;
-    const int c = lslot ^ ((r >> 2) & 3);
+    const int c = lslot ^ swz<CPR>(r);
     boff[j] = (i < BI && n < a.N) ? n * a.ldb * 2 + c * 16 : OOB;
   }
 
@@ -587,7 +598,7 @@ __global__ __launch_bounds__(256, MINB) void gemm_bf16_dma_kernel(GemmArgs a) {
     bf16* bdst = &Bs[stg][0];
 #pragma unroll
     for (int j = 0; j < BW; ++j) {
-      const int i = wave + 4 * j;
+      const int i = wave + NWV * j;
       if (i < BI)  // wave-uniform
         dma16(bres, bdst + i * 512, boff[j] == OOB ? OOB : boff[j] + 2 * k0);
     }
@@ -629,12 +640,12 @@ __global__ __launch_bounds__(256, MINB) void gemm_bf16_dma_kernel(GemmArgs a) {
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int r = arow + i * 32;
-        af[i] = *reinterpret_cast<const bf16x8*>(&Ab[r * DK + 8 * (ch ^ ((r >> 2) & 3))]);
+        af[i] = *reinterpret_cast<const bf16x8*>(&Ab[r * DK + 8 * (ch ^ swz<CPR>(r))]);
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int r = brow + j * 32;
-        bfr[j] = *reinterpret_cast<const bf16x8*>(&Bb[r * DK + 8 * (ch ^ ((r >> 2) & 3))]);
+        bfr[j] = *reinterpret_cast<const bf16x8*>(&Bb[r * DK + 8 * (ch ^ swz<CPR>(r))]);
       }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
@@ -792,16 +803,16 @@ static void launch_bf16(const GemmArgs& a, hipStream_t s) {
 
 // Direct-to-LDS kernel for the uniform-tap modes; false if the layer needs
 // the register-staged loader.
-template <int BM, int BN, int WM, int WN, int DNS, int MINB>
+template <int BM, int BN, int WM, int WN, int DNS, int MINB, int DK = DKS>
 static bool launch_dma(const GemmArgs& a, hipStream_t s) {
   const int mode = loader_mode(a, DK);
-  if (mode == 0) return false;
+  if (mode == 0 || (DK != DKS && a.ksplit > 1)) return false;
   const long blocks = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN) * a.ksplit;
-  const dim3 g((unsigned)blocks), b(256);
+  const dim3 g((unsigned)blocks), b(64 * WM * WN);
   if (mode == 1)
-    gemm_bf16_dma_kernel<BM, BN, WM, WN, 1, DNS, MINB><<<g, b, 0, s>>>(a);
+    gemm_bf16_dma_kernel<BM, BN, WM, WN, 1, DNS, MINB, DK><<<g, b, 0, s>>>(a);
   else
-    gemm_bf16_dma_kernel<BM, BN, WM, WN, 2, DNS, MINB><<<g, b, 0, s>>>(a);
+    gemm_bf16_dma_kernel<BM, BN, WM, WN, 2, DNS, MINB, DK><<<g, b, 0, s>>>(a);
   if (a.ksplit > 1) {
     const long n = (long)a.M * (a.N / 4);
     splitk_reduce_kernel<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s>>>(a);
@@ -819,7 +830,7 @@ int gemm_ksplit(const GemmArgs& a) {
   const long hw = (long)a.seg[0].Ho * a.seg[0].Wo;
   if (a.seg[0].ks != 3 || a.K < 5120 || hw > 256 || a.N % 160 || a.epi.geglu || a.epi.vt_out || a.epi.out_f32)
     return 1;
-  if (loader_mode(a, DK) == 0) return 1;
+  if (loader_mode(a, DKS) == 0) return 1;
   return hw <= 64 ? 4 : 2;
 }
 
@@ -833,7 +844,7 @@ hipError_t launch_gemm(DType dt, const GemmArgs& args, hipStream_t s) {
   if (a.ksplit < 1) a.ksplit = 1;
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   if (a.ksplit > 1 && (dt != BF16 || !a.partial || a.epi.geglu || a.epi.vt_out || a.epi.out_f32 ||
-                       a.N % 160 || loader_mode(a, DK) == 0))
+                       a.N % 160 || loader_mode(a, DKS) == 0))
     return hipErrorInvalidValue;
   if (dt == BF16 && (a.N % 4 || a.epi.ldo % 4 || (a.epi.resid && a.epi.ldr % 4) || (a.epi.geglu && a.N % 32) ||
                      a.epi.qcols % 4))
@@ -846,10 +857,12 @@ hipError_t launch_gemm(DType dt, const GemmArgs& args, hipStream_t s) {
     auto nblk = [&](int bm, int bn) { return (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn); };
     const long want = 2 * 256;
     if (a.N % 160 == 0) {
-      // 256x160 tiles through the direct-to-LDS pipeline when the loader is
-      // uniform; otherwise register-staged 64-deep tiles, one block per CU.
+      // 256x160 tiles through the two-stage direct-to-LDS pipeline whenever
+      // the loader is uniform: taller tiles cut the weight re-reads that
+      // dominate small-M layers, and two stages leave LDS for two blocks.
+      // Otherwise register-staged 64-deep tiles, one block per CU.
       const bool big = nblk(256, 160) * a.ksplit >= want;
-      if (big ? launch_dma<256, 160, 4, 1, 3, 2>(a, s) : launch_dma<128, 160, 4, 1, 3, 2>(a, s)) {
+      if (launch_dma<256, 160, 4, 1, 2, 2>(a, s)) {
       } else if (big) {
         launch_bf16<256, 160, 64, 4, 1>(a, s);
       } else {
