@@ -214,6 +214,106 @@ __device__ __forceinline__ void epilogue_tiles(const GemmArgs& a, const f32x16 (
   });
 }
 
+// Epilogue through LDS for bf16 outputs with no transposed part: each wave
+// finishes its values in registers (bias, time bias, GEGLU, residual, query
+// scale), writes 32 rows of its tile as bf16 into a private LDS region, then
+// stores them back row-contiguous, 16 bytes per lane, so a wave writes whole
+// runs instead of 32 scattered 8-byte pieces.  A residual is first copied
+// into the same region row-contiguous, and each lane picks up its own
+// elements there before overwriting them with the result (one rounding).
+// Row stride of the region: the wave's columns plus 8 (16 bytes), which
+// keeps rows 16-byte aligned and the 8-byte writes of 32 consecutive rows at
+// most two to a bank.
+template <int OW>
+constexpr int STAGED_LD = OW + 8;
+
+template <int BM, int BN, int WM, int WN, int TM, int TN>
+__device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int m0, int n0,
+                                                int wm, int wn, int lane, bf16* R) {
+  constexpr int WC = BN / WN;  // the wave's accumulator columns
+  constexpr int LD = STAGED_LD<WC>;
+  const Epi& e = a.epi;
+  const bool geglu = e.geglu;
+  const int OW = geglu ? WC / 2 : WC;  // output columns of the wave
+  const int ncol0 = (geglu ? n0 / 2 : n0) + wn * OW;
+  const int lr = lane & 31, hq = 4 * (lane >> 5);
+  const int cpr = OW / 8;  // 16-byte chunks per row
+  const bf16* resid = reinterpret_cast<const bf16*>(e.resid);
+  static_for<0, TM>([&](auto I) {
+    const int mrow0 = m0 + wm * (BM / WM) + I.value * 32;
+    if (resid) {  // (not with GEGLU)
+      for (int c = lane; c < 32 * cpr; c += 64) {
+        const int row = c / cpr, ch = c - row * cpr;
+        const int m = mrow0 + row;
+        bf16x8 r = {};
+        if (m < a.M) r = *reinterpret_cast<const bf16x8*>(resid + (long)m * e.ldr + ncol0 + ch * 8);
+        *reinterpret_cast<bf16x8*>(R + row * LD + ch * 8) = r;
+      }
+      asm volatile("" ::: "memory");  // (one wave's LDS accesses complete in order)
+    }
+    static_for<0, TN>([&](auto J) {
+      const f32x16 v = acc[I.value][J.value];
+      const int nt = n0 + wn * WC + J.value * 32;
+      const int m = mrow0 + lr;
+      if (geglu) {
+        // packed columns 32t + u (a) and 32t + 16 + u (gate) -> channel 16t + u
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const int n = nt + 8 * q + hq;
+          float x[4];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const float av = v[4 * q + k] + e.bias[n + k];
+            const float g = v[4 * (q + 2) + k] + e.bias[n + 16 + k];
+            x[k] = av * (0.5f * g * (1.0f + erff(g * 0.70710678118654752f)));
+          }
+          bf16x4 o;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) o[k] = (bf16)x[k];
+          *reinterpret_cast<bf16x4*>(R + lr * LD + J.value * 16 + 8 * q + hq) = o;
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int n = nt + 8 * q + hq;
+          float x[4] = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+          if (e.bias) {
+            const float4 b = *reinterpret_cast<const float4*>(e.bias + n);
+            x[0] += b.x; x[1] += b.y; x[2] += b.z; x[3] += b.w;
+          }
+          if (e.tbias && m < a.M) {
+            const float4 b = *reinterpret_cast<const float4*>(e.tbias + (long)(m / e.hw) * e.tb_ld + e.tb_off + n);
+            x[0] += b.x; x[1] += b.y; x[2] += b.z; x[3] += b.w;
+          }
+          bf16* slot = R + lr * LD + J.value * 32 + 8 * q + hq;
+          if (resid) {
+            const bf16x4 r = *reinterpret_cast<const bf16x4*>(slot);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) x[k] += (float)r[k];
+          }
+          if (n < e.qcols) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) x[k] *= e.qscale;
+          }
+          bf16x4 o;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) o[k] = (bf16)x[k];
+          *reinterpret_cast<bf16x4*>(slot) = o;
+        }
+      }
+    });
+    asm volatile("" ::: "memory");
+    for (int c = lane; c < 32 * cpr; c += 64) {
+      const int row = c / cpr, ch = c - row * cpr;
+      const int m = mrow0 + row;
+      if (m < a.M && ncol0 + ch * 8 < (geglu ? a.N / 2 : a.N))
+        *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(e.out) + (long)m * e.ldo + ncol0 + ch * 8) =
+            *reinterpret_cast<const bf16x8*>(R + row * LD + ch * 8);
+    }
+    asm volatile("" ::: "memory");
+  });
+}
+
 // Loader modes.
 //  0: per-thread addressing of any layer (incl. the GroupNorm affine on load).
 //  1: every segment is a stride-1 3x3 or 1x1 layer on an image of the
@@ -474,8 +574,11 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
   static_assert(DNS >= 2 && DNS <= 4, "pipeline depth");
   static_assert(DK == 32 || DK == 64, "stage depth");
   static_assert(AI % NWV == 0, "A tile must split evenly over the waves");
-  __shared__ __attribute__((aligned(1024))) bf16 As[DNS][BM * DK];
-  __shared__ __attribute__((aligned(1024))) bf16 Bs[DNS][BN * DK];
+  // Operand stages (A then B); after the K loop the same LDS stages the
+  // output tile for the row-contiguous stores of the epilogue.
+  __shared__ __attribute__((aligned(1024))) bf16 smem[DNS * (BM + BN) * DK];
+  bf16* const As = smem;
+  bf16* const Bs = smem + DNS * BM * DK;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int tiles_n = (a.N + BN - 1) / BN;
@@ -558,7 +661,7 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
     }
     const bool in0 = cb < gc0;
     const int cs = in0 ? gc0 : gc1, cbase = 2 * (in0 ? cb : cb - gc0);
-    bf16* adst = &As[stg][0];
+    bf16* adst = As + stg * BM * DK;
     if constexpr (MODE == 1) {
       const __amdgpu_buffer_rsrc_t ares = make_rsrc(in0 ? gs0 : gs1, (long)a.M * cs * 2);
       const int t9 = gks == 3 ? tap : 4;
@@ -595,7 +698,7 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
         dma16(ares, adst + (wave * AW + j) * 512, off);
       }
     }
-    bf16* bdst = &Bs[stg][0];
+    bf16* bdst = Bs + stg * BN * DK;
 #pragma unroll
     for (int j = 0; j < BW; ++j) {
       const int i = wave + NWV * j;
@@ -631,8 +734,8 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
     asm volatile("" ::: "memory");  // the LDS was written behind the compiler's back
     __syncthreads();
     if (kt + DNS - 1 < nk) issue(kb + kt + DNS - 1, (kt + DNS - 1) % DNS);
-    const bf16* Ab = As[kt % DNS];
-    const bf16* Bb = Bs[kt % DNS];
+    const bf16* Ab = As + (kt % DNS) * BM * DK;
+    const bf16* Bb = Bs + (kt % DNS) * BN * DK;
 #pragma unroll
     for (int ks = 0; ks < DK / 16; ++ks) {
       const int ch = 2 * ks + lh;
@@ -674,6 +777,12 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
         }
       });
     });
+    return;
+  }
+  static_assert(NWV * 32 * STAGED_LD<BN / WN> <= DNS * (BM + BN) * DK, "staging fits the operand stages");
+  if (!a.epi.vt_out && !a.epi.out_f32 && (!a.epi.resid || !a.epi.geglu)) {
+    __syncthreads();  // every wave is done with the operand stages
+    epilogue_staged<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane, smem + wave * 32 * STAGED_LD<BN / WN>);
     return;
   }
   epilogue_tiles<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane);

@@ -74,11 +74,12 @@ CONV_CASES = [
 ]
 
 
+@pytest.mark.parametrize("with_resid", [True, False])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("case", CONV_CASES)
-def test_conv(ops, dt, case):
+def test_conv(ops, dt, case, with_resid):
     n, H, W, c0, c1, cout, ks, stride, up, aff = case
-    log(f"conv {dt} {case}")
+    log(f"conv {dt} {case} resid={with_resid}")
     rng = np.random.default_rng(hash(case) % 2**32)
     x0 = _vals(rng, (n, H, W, c0), dt)
     x1 = _vals(rng, (n, H, W, c1), dt) if c1 else None
@@ -94,7 +95,7 @@ def test_conv(ops, dt, case):
     got = ops.conv(_dev(x0, dt), _dev(_pack(w), dt), cout, ks, stride, up,
                    x1=_dev(x1, dt) if c1 else None,
                    scale=_dev(scale) if aff else None, shift=_dev(shift) if aff else None, silu=int(aff),
-                   bias=_dev(b), resid=None if out_f32 else _dev(res, dt), out_f32=out_f32)
+                   bias=_dev(b), resid=_dev(res, dt) if with_resid and not out_f32 else None, out_f32=out_f32)
     torch.cuda.synchronize()
     got = got.float().cpu().numpy()
     for i in range(n):
@@ -103,7 +104,7 @@ def test_conv(ops, dt, case):
             a = O.silu(a * scale[i] + shift[i])
         if up:
             a = O.upsample_nearest2x(a)
-        ref = O.conv2d(a, w, b, stride) + (0 if out_f32 else res[i])
+        ref = O.conv2d(a, w, b, stride) + (res[i] if with_resid and not out_f32 else 0)
         err = rel_l2(got[i], ref)
         assert err <= TOL[dt], (i, err)
 
