@@ -326,14 +326,6 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 
 // Modes 1 and 2 read through buffer resources: a masked-off element gets an
 // out-of-range offset, which the hardware returns as zero, so the loads are
 // branch-free.
-constexpr int OOB = (int)0x80000000u;
-
-__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, long bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
-}
-__device__ inline bf16x8 buf_load16(__amdgpu_buffer_rsrc_t r, int off) {
-  return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
-}
 
 template <int BM, int BN, int BK, int WM, int WN, int MODE, int MINB>
 __global__ __launch_bounds__(256, MINB) void gemm_bf16_kernel(GemmArgs a) {
@@ -545,22 +537,6 @@ constexpr int DKS = 32;  // K depth per stage (the split-K and loader-mode granu
 template <int CPR>
 __device__ __forceinline__ int swz(int r) {
   return CPR == 4 ? (r >> 2) & 3 : (r >> 1) & 7;
-}
-
-// One 16-byte-per-lane direct-to-LDS load (64 lanes -> 1 KB at `lds`).
-// The builtin exists only for the device pass; the host pass of this file
-// compiles the kernels' launch stubs and never runs this body.
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, bf16* lds, int off) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, off, 0, 0, 0);
-#endif
-}
-
-template <int WAITN>
-__device__ __forceinline__ void wait_vmcnt() {
-  // s_waitcnt with only the vector-memory counter limited to WAITN
-  static_assert(WAITN >= 0 && WAITN < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((WAITN & 15) | (7 << 4) | (15 << 8) | ((WAITN >> 4) << 14));
 }
 
 template <int BM, int BN, int WM, int WN, int MODE, int DNS, int MINB, int DK>

@@ -117,6 +117,9 @@ def test_conv(ops, dt, case, with_resid):
     (8, 80, 160, 160, 1.0, False), (8, 160, 64, 64, 1.0, False), (8, 160, 90, 77, 1.0, True),
     (2, 40, 36, 36, 1.0, False), (2, 24, 130, 130, 1.0, False), (1, 48, 64, 200, 30.0, True),
     (4, 56, 65, 129, 1.0, False), (2, 72, 100, 100, 1.0, False), (2, 128, 70, 70, 1.0, False),
+    # key counts in whole 8-key chunks take the direct-to-LDS tiles (partial last tile, folded max)
+    (8, 40, 130, 256, 1.0, False), (2, 24, 100, 64, 30.0, True), (8, 40, 64, 200, 1.0, True),
+    (4, 56, 96, 136, 1.0, False), (8, 40, 32, 8, 1.0, True), (2, 64, 70, 520, 30.0, False),
 ])
 def test_attention(ops, dt, qmode, heads, d, nq, nk, scale, cross):
     """bf16 takes V transposed (channel-major, padded token stride, as the
