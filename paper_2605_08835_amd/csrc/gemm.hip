@@ -314,6 +314,40 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 
   });
 }
 
+// The transposed part of a QKV projection (V written [image][channel][token]
+// for the attention kernel): the wave stages its 32 tokens x WC channels
+// channel-major, then stores 16-byte runs of 8 consecutive tokens.  Needs
+// the 32 tokens in one image at a multiple of 32 (vt_hw % 32 == 0) and
+// 16-byte aligned channel rows (vt_ld % 8 == 0).
+template <int BM, int BN, int WM, int WN, int TM, int TN>
+__device__ __forceinline__ void epilogue_staged_vt(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int m0, int n0,
+                                                   int wm, int wn, int lane, bf16* R) {
+  constexpr int WC = BN / WN;
+  const Epi& e = a.epi;
+  const int lr = lane & 31, hq = 4 * (lane >> 5);
+  const int c0 = n0 + wn * WC - e.vt_col0;  // first V channel of the wave
+  static_for<0, TM>([&](auto I) {
+    const int mrow0 = m0 + wm * (BM / WM) + I.value * 32;
+    static_for<0, TN>([&](auto J) {
+      const f32x16 v = acc[I.value][J.value];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) R[(J.value * 32 + 8 * q + hq + k) * 32 + lr] = (bf16)v[4 * q + k];
+    });
+    asm volatile("" ::: "memory");  // (one wave's LDS accesses complete in order)
+    const int img = mrow0 / e.vt_hw, tok0 = mrow0 - img * e.vt_hw;
+    bf16* dst = reinterpret_cast<bf16*>(e.vt_out) + (long)img * e.vt_img + (long)c0 * e.vt_ld + tok0;
+    for (int c = lane; c < WC * 4; c += 64) {
+      const int ch = c >> 2, part = c & 3;
+      if (mrow0 + 8 * part < a.M)  // (M is a multiple of vt_hw, hence of 32)
+        *reinterpret_cast<bf16x8*>(dst + (long)ch * e.vt_ld + 8 * part) =
+            *reinterpret_cast<const bf16x8*>(R + ch * 32 + 8 * part);
+    }
+    asm volatile("" ::: "memory");
+  });
+}
+
 // Loader modes.
 //  0: per-thread addressing of any layer (incl. the GroupNorm affine on load).
 //  1: every segment is a stride-1 3x3 or 1x1 layer on an image of the
@@ -756,9 +790,15 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
     return;
   }
   static_assert(NWV * 32 * STAGED_LD<BN / WN> <= DNS * (BM + BN) * DK, "staging fits the operand stages");
-  if (!a.epi.vt_out && !a.epi.out_f32 && (!a.epi.resid || !a.epi.geglu)) {
+  static_assert(32 * (BN / WN) <= 32 * STAGED_LD<BN / WN>, "transposed staging fits the region");
+  const bool vt_ok = a.epi.vt_out && a.epi.vt_col0 % (BN / WN) == 0 && a.epi.vt_hw % 32 == 0 && a.epi.vt_ld % 8 == 0;
+  if ((!a.epi.vt_out || vt_ok) && !a.epi.out_f32 && (!a.epi.resid || !a.epi.geglu)) {
     __syncthreads();  // every wave is done with the operand stages
-    epilogue_staged<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane, smem + wave * 32 * STAGED_LD<BN / WN>);
+    bf16* R = smem + wave * 32 * STAGED_LD<BN / WN>;
+    if (a.epi.vt_out && n0 + wn * (BN / WN) >= a.epi.vt_col0)
+      epilogue_staged_vt<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane, R);
+    else
+      epilogue_staged<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane, R);
     return;
   }
   epilogue_tiles<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane);
