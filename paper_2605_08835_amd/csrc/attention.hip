@@ -163,7 +163,7 @@ __device__ __forceinline__ void softmax_tile(f32x16 (&s)[2], f32x16 (&o)[ND], bf
 // in row d of the PV product.  V is stored transposed per image
 // ([channel][token], as the projection GEMM writes it), so a V^T tile is
 // staged with 16-byte loads and stores.
-template <int D16, bool QS, bool MF, bool SF, int NW>
+template <int D16, bool QS, bool MF, bool SF, int NW, int QG>
 __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(AttnArgs a) {
   using namespace fa;
   static_assert(QS || !MF, "the max can ride in the product only with pre-scaled queries");
@@ -177,7 +177,7 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
   __shared__ __attribute__((aligned(16))) bf16 Vt[2][DP * LDV];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int img = blockIdx.z, head = blockIdx.y;
-  const int qb = blockIdx.x * (32 * NW) + wave * 32;
+  const int qb = blockIdx.x * (32 * NW * QG) + wave * (32 * QG);
   const int kvimg = a.kv_index ? a.kv_index[img] : img;
   const int hd = head * a.d;
   const bf16* Q = reinterpret_cast<const bf16*>(a.q) + (long)img * a.q_img + hd;
@@ -189,22 +189,28 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
 
   // Q^T fragment (B operand): query qb + lq, head dims 16 j + 8 lh + [0, 8);
   // column d (when MF) holds -m.
-  bf16x8 qf[NJ];
-  {
-    const int q = qb + lq;
+  // QG groups of 32 queries per wave share every K and V fragment read.
+  bf16x8 qf[QG][NJ];
+#pragma unroll
+  for (int g = 0; g < QG; ++g) {
+    const int q = qb + 32 * g + lq;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
       const int dd = 16 * j + 8 * lh;
       const bf16x8 z = {};
-      qf[j] = (q < a.Nq && dd < d) ? ld16(Q + (long)q * a.q_ld + dd) : z;
+      qf[g][j] = (q < a.Nq && dd < d) ? ld16(Q + (long)q * a.q_ld + dd) : z;
     }
   }
-  f32x16 o[ND];
+  f32x16 o[QG][ND];
 #pragma unroll
-  for (int t = 0; t < ND; ++t)
+  for (int g = 0; g < QG; ++g)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) o[t][r] = 0.f;
-  float m_run = 0.f, l_run = 0.f;
+    for (int t = 0; t < ND; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[g][t][r] = 0.f;
+  float m_run[QG], l_run[QG];
+#pragma unroll
+  for (int g = 0; g < QG; ++g) m_run[g] = l_run[g] = 0.f;
   const bool vvec = (a.v_ld & 7) == 0;
 
   bf16x8 rk[KPT], rv[VPT];
@@ -274,27 +280,34 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
     const bf16* Vb = Vt[b];
 
     // S^T tiles: rows = keys kt*32 + 8(r/4) + 4 lh + r%4, col = query.
-    f32x16 s[2];
+    f32x16 s[QG][2];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int g = 0; g < QG; ++g)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[kt][r] = 0.f;
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[g][kt][r] = 0.f;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
         const bf16x8 kf = ld16(&Kb[(kt * 32 + lq) * LDK + 16 * j + 8 * lh]);
-        s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[j], s[kt], 0, 0, 0);
+#pragma unroll
+        for (int g = 0; g < QG; ++g) s[g][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[g][j], s[g][kt], 0, 0, 0);
       }
-    softmax_tile<NJ, ND, QS, MF, SF, TAIL>(s, o, qf, m_run, l_run, it == 0, a.Nk - k0, lh, d, sl2);
+#pragma unroll
+    for (int g = 0; g < QG; ++g)
+      softmax_tile<NJ, ND, QS, MF, SF, TAIL>(s[g], o[g], qf[g], m_run[g], l_run[g], it == 0, a.Nk - k0, lh, d, sl2);
 
     // O^T += V^T P^T over four 16-key slices.  Slot (lh, i) of slice u is
     // key 16u + 8(i/4) + 4 lh + i%4, i.e. register 8(u%2) + i of S^T tile u/2.
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      bf16x8 pf;
+      bf16x8 pf[QG];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) pf[i] = (bf16)s[u >> 1][8 * (u & 1) + i];
+      for (int g = 0; g < QG; ++g)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) pf[g][i] = (bf16)s[g][u >> 1][8 * (u & 1) + i];
 #pragma unroll
       for (int t = 0; t < ND; ++t) {
         const bf16* vrow = &Vb[(t * 32 + lq) * LDV + 16 * u + 4 * lh];
@@ -303,7 +316,8 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
         bf16x8 vf;
         vf[0] = lo[0]; vf[1] = lo[1]; vf[2] = lo[2]; vf[3] = lo[3];
         vf[4] = hi[0]; vf[5] = hi[1]; vf[6] = hi[2]; vf[7] = hi[3];
-        o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[t], 0, 0, 0);
+#pragma unroll
+        for (int g = 0; g < QG; ++g) o[g][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[g], o[g][t], 0, 0, 0);
       }
     }
     if (more) stage(b ^ 1);
@@ -315,31 +329,34 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
 
   // O^T accumulator: lane holds head dims t*32 + 8(r/4) + 4 lh + [0, 4) of
   // its query; each run of 4 is one 8-byte store.
-  float l = l_run;
-  if constexpr (SF) {  // the ones row d of V^T accumulated the row sum into O^T row d
-    l = 0.f;
 #pragma unroll
-    for (int t = 0; t < ND; ++t)
+  for (int g = 0; g < QG; ++g) {
+    float l = l_run[g];
+    if constexpr (SF) {  // the ones row d of V^T accumulated the row sum into O^T row d
+      l = 0.f;
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        if (32 * t + 8 * (r >> 2) + 4 * lh + (r & 3) == d) l = o[t][r];
-  }
-  const float inv = 1.0f / xor32_sum(l);
-  const int q = qb + lq;
-  if (q < a.Nq) {
-    bf16* O = reinterpret_cast<bf16*>(a.o) + (long)img * a.o_img + (long)q * a.o_ld + hd;
+      for (int t = 0; t < ND; ++t)
 #pragma unroll
-    for (int t = 0; t < ND; ++t)
+        for (int r = 0; r < 16; ++r)
+          if (32 * t + 8 * (r >> 2) + 4 * lh + (r & 3) == d) l = o[g][t][r];
+    }
+    const float inv = 1.0f / xor32_sum(l);
+    const int q = qb + 32 * g + lq;
+    if (q < a.Nq) {
+      bf16* O = reinterpret_cast<bf16*>(a.o) + (long)img * a.o_img + (long)q * a.o_ld + hd;
 #pragma unroll
-      for (int rg = 0; rg < 4; ++rg) {
-        const int dd = t * 32 + 8 * rg + 4 * lh;
-        if (dd < d) {
-          bf16x4 w;
+      for (int t = 0; t < ND; ++t)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) w[e] = (bf16)(o[t][4 * rg + e] * inv);
-          *reinterpret_cast<bf16x4*>(O + dd) = w;
+        for (int rg = 0; rg < 4; ++rg) {
+          const int dd = t * 32 + 8 * rg + 4 * lh;
+          if (dd < d) {
+            bf16x4 w;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) w[e] = (bf16)(o[g][t][4 * rg + e] * inv);
+            *reinterpret_cast<bf16x4*>(O + dd) = w;
+          }
         }
-      }
+    }
   }
 }
 
@@ -397,9 +414,11 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
 
 template <int D16, bool QS, bool MF, bool SF>
 static void launch_d(const AttnArgs& a, hipStream_t s) {
-  constexpr int NW = 4;
-  dim3 grid((a.Nq + 32 * NW - 1) / (32 * NW), a.heads, a.imgs);
-  attn_bf16_kernel<D16, QS, MF, SF, NW><<<grid, 64 * NW, 0, s>>>(a);
+  // Narrow heads take two query groups per wave (half the K/V traffic and
+  // fragment reads per query, still two waves per SIMD); wider ones one.
+  constexpr int NW = 4, QG = D16 <= 64 ? 2 : 1;
+  dim3 grid((a.Nq + 32 * NW * QG - 1) / (32 * NW * QG), a.heads, a.imgs);
+  attn_bf16_kernel<D16, QS, MF, SF, NW, QG><<<grid, 64 * NW, 0, s>>>(a);
 }
 
 // Head widths d (multiples of 8) whose 16-rounding is D16: d = D16 - 8
