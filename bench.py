@@ -24,10 +24,21 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 WORKLOAD = "c3_sd15_mixed32"
+# Other single-GPU workloads bench.py can time with --workload (the default
+# line is the one above): algorithmic FLOPs per UNet row and a description.
+WORKLOADS = {
+    "c3_sd15_mixed32": (803.27e9, "SD-1.5-shaped UNet, latent 4x64x64, bf16; 32 requests at seeded timesteps, "
+                                  "16 under Skip-CFG -> 48 packed rows; guidance U[5,9]; 77x768 contexts; "
+                                  "UNet + CFG combine + DDIM per step"),
+    "c2_sd15_cfg8": (803.27e9, "SD-1.5-shaped UNet, latent 4x64x64, bf16; 8 requests, all with CFG -> 16 rows; "
+                               "guidance 7.5; 77x768 contexts; UNet + CFG combine + DDIM per step"),
+    "c4_sdxl_cfg8": (6761.24e9, "SDXL-shaped UNet, latent 4x128x128, bf16, channels 320/640/1280, "
+                                "transformer depths 0/2/10, 64-wide heads; 8 requests, all with CFG -> 16 rows; "
+                                "77x2048 contexts, pooled 1280 + 6 time ids; UNet + CFG combine + DDIM per step"),
+}
 METRIC = "UNet rows·steps/sec + % bf16 MFMA peak, SD-1.5-shape, 32-req mixed-CFG batch"
 PEAK_BF16 = 2.5166e15  # dense bf16 MFMA, 256 CU x 4096 FLOP/clk x 2.4 GHz
 PEAK_HBM = 8.0e12
-FLOP_PER_ROW = 803.27e9  # algorithmic FLOPs of one SD-1.5 UNet evaluation at 64x64
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_sd15_48rows_traffic.md")
@@ -153,7 +164,7 @@ def cpu_baseline(unet, weights, req, budget_s=25.0):
             break
     el = time.perf_counter() - t0
     return {"value": rows / el, "unit": "rows·steps/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"{len(done)} requests ({rows} UNet rows) of the same 32-request batch, "
+            "sample": f"{len(done)} requests ({rows} UNet rows) of the same {len(req['cfg_on'])}-request batch, "
                       f"one full float64 step each, {el:.1f} s"}
 
 
@@ -164,6 +175,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layers", default=None, help="write a per-layer device-time table to this file")
+    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(WORKLOADS),
+                    help="batch to time (the default is the metric's workload)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="run a plain copy kernel of MIB MiB each way first (counter calibration)")
     ap.add_argument("--summarize", nargs="*", metavar="DIR",
@@ -184,11 +197,13 @@ def main():
     from fixtures import get_config, make_requests, make_weights
     from paper_2605_08835_amd import UNet
 
-    spec = get_config(WORKLOAD)
+    wl = args.workload
+    flop_per_row, description = WORKLOADS[wl]
+    spec = get_config(wl)
     unet = spec["unet"]
     t0 = time.time()
-    weights = make_weights(WORKLOAD)
-    req = make_requests(WORKLOAD)
+    weights = make_weights(wl)
+    req = make_requests(wl)
     log(f"inputs ready in {time.time() - t0:.1f} s")
     R = len(req["timesteps"])
     rows = int(R + req["cfg_on"].sum())
@@ -210,8 +225,15 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    extra = {}
+    if "pooled_cond" in req:  # SDXL-style added conditioning
+        extra = dict(pooled_cond=torch.from_numpy(np.asarray(req["pooled_cond"], np.float32)).to(dev),
+                     pooled_uncond=torch.from_numpy(np.asarray(req["pooled_uncond"], np.float32)).to(dev),
+                     time_ids=req["time_ids"])
+
     def step():
-        m.step(lat, req["timesteps"], req["cfg_on"], req["guidance"], ctx, unc, coef, out=out, stream=stream)
+        m.step(lat, req["timesteps"], req["cfg_on"], req["guidance"], ctx, unc, coef, out=out, stream=stream,
+               **extra)
 
     for _ in range(args.warmup):
         step()
@@ -258,7 +280,7 @@ def main():
     achieved = flop_per_launch / avg_s / 1e12
     roof = {"kernel": "gemm_bf16_kernel (implicit-GEMM conv / linear, MFMA 32x32x16 bf16)",
             "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
-            "frac": round(achieved * 1e12 / PEAK_BF16, 4), "traffic": stored_traffic(),
+            "frac": round(achieved * 1e12 / PEAK_BF16, 4), "traffic": stored_traffic() if wl == WORKLOAD else None,
             "flop_per_launch": flop_per_launch, "launches_per_step": g_launches,
             "avg_launch_us": round(avg_s * 1e6, 2)}
 
@@ -268,16 +290,16 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) latents and contexts, random-init N(0,0.02) weights)",
-        "config": {"workload": "SD-1.5-shaped UNet, latent 4x64x64, bf16; 32 requests at seeded "
-                               "timesteps, 16 under Skip-CFG -> 48 packed rows; guidance U[5,9]; "
-                               "77x768 contexts; UNet + CFG combine + DDIM per step",
-                   "requests": R, "rows": rows, "latent": [4, 64, 64]},
+        "config": {"workload": description, "name": wl, "requests": R, "rows": rows,
+                   "latent": [unet["latent_c"], unet["latent_h"], unet["latent_w"]]},
         "requests_steps_per_s": round(R * 1e3 / ms, 2),
-        "pct_bf16_peak": round(100 * value * FLOP_PER_ROW / PEAK_BF16, 2),
+        "pct_bf16_peak": round(100 * value * flop_per_row / PEAK_BF16, 2),
         "roofline": roof,
         "kernels": kernels,
     }
-    if not args.no_cpu_baseline:
+    if wl != WORKLOAD:
+        res["metric"] = METRIC.replace("SD-1.5-shape, 32-req mixed-CFG batch", wl)
+    if not args.no_cpu_baseline and wl == WORKLOAD:
         log("timing the CPU oracle on a bounded sample ...")
         res["cpu_baseline"] = cpu_baseline(unet, weights, req)
     m.close()

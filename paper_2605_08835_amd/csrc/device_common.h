@@ -40,6 +40,24 @@ template <typename T> __device__ inline T from_f(float x) { return (T)x; }
 
 __device__ inline float silu_f(float x) { return x / (1.0f + __expf(-x)); }
 
+// GELU(x) = x Phi(x), Phi(x) = (1 + erf(x / sqrt 2)) / 2, with erf from
+// Abramowitz & Stegun 7.1.26 (absolute error below 1.5e-7, far under a
+// bf16 rounding): for u >= 0, 1 - erf(u) = t (a1 + t (a2 + t (a3 + t (a4 +
+// t a5)))) exp(-u^2), t = 1 / (1 + p u).  A reciprocal and an exp2 are its
+// only transcendental instructions, against a library erff's piecewise
+// polynomials; the bf16 GEGLU epilogues use it.
+__device__ inline float gelu_as(float x) {
+  const float u = fabsf(x) * 0.70710678118654752f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, u, 1.0f));
+  float p = fmaf(t, 1.061405429f, -1.453152027f);
+  p = fmaf(t, p, 1.421413741f);
+  p = fmaf(t, p, -0.284496736f);
+  p = fmaf(t, p, 0.254829592f);
+  // h = (1 - erf(u)) / 2; exp(-u^2) = exp2(-x^2 log2(e) / 2)
+  const float h = 0.5f * t * p * __builtin_amdgcn_exp2f(x * x * -0.72134752044448170f);
+  return x * (x >= 0.f ? 1.0f - h : h);
+}
+
 __device__ inline float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

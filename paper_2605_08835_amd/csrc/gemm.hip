@@ -185,7 +185,7 @@ __device__ __forceinline__ void epilogue_tiles(const GemmArgs& a, const f32x16 (
               for (int e = 0; e < 4; ++e) {
                 x[e] = v[4 * q + e] + a.epi.bias[n + e];
                 g[e] = v[4 * (q + 2) + e] + a.epi.bias[n + 16 + e];
-                x[e] *= 0.5f * g[e] * (1.0f + erff(g[e] * 0.70710678118654752f));
+                x[e] *= gelu_as(g[e]);
               }
               store4<bf16>(a.epi, m, nt / 2 + 8 * q + hq, x);
             }
@@ -265,7 +265,7 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 
           for (int k = 0; k < 4; ++k) {
             const float av = v[4 * q + k] + e.bias[n + k];
             const float g = v[4 * (q + 2) + k] + e.bias[n + 16 + k];
-            x[k] = av * (0.5f * g * (1.0f + erff(g * 0.70710678118654752f)));
+            x[k] = av * gelu_as(g);
           }
           bf16x4 o;
 #pragma unroll
