@@ -586,7 +586,8 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
   static_assert(AI % NWV == 0, "A tile must split evenly over the waves");
   // Operand stages (A then B); after the K loop the same LDS stages the
   // output tile for the row-contiguous stores of the epilogue.
-  __shared__ __attribute__((aligned(1024))) bf16 smem[DNS * (BM + BN) * DK];
+  constexpr int OPS = DNS * (BM + BN) * DK, STG = NWV * 32 * STAGED_LD<BN / WN>;
+  __shared__ __attribute__((aligned(1024))) bf16 smem[OPS > STG ? OPS : STG];
   bf16* const As = smem;
   bf16* const Bs = smem + DNS * BM * DK;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -789,7 +790,6 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
     });
     return;
   }
-  static_assert(NWV * 32 * STAGED_LD<BN / WN> <= DNS * (BM + BN) * DK, "staging fits the operand stages");
   static_assert(32 * (BN / WN) <= 32 * STAGED_LD<BN / WN>, "transposed staging fits the region");
   const bool vt_ok = a.epi.vt_out && a.epi.vt_col0 % (BN / WN) == 0 && a.epi.vt_hw % 32 == 0 && a.epi.vt_ld % 8 == 0;
   if ((!a.epi.vt_out || vt_ok) && !a.epi.out_f32 && (!a.epi.resid || !a.epi.geglu)) {
@@ -987,7 +987,9 @@ hipError_t launch_gemm(DType dt, const GemmArgs& args, hipStream_t s) {
       // dominate small-M layers, and two stages leave LDS for two blocks.
       // Otherwise register-staged 64-deep tiles, one block per CU.
       const bool big = nblk(256, 160) * a.ksplit >= want;
-      if (launch_dma<256, 160, 4, 1, 2, 2>(a, s)) {
+      if (a.ksplit == 1 && nblk(256, 160) < 256 && launch_dma<64, 160, 2, 1, 2, 4>(a, s)) {
+        // short M (the context K/V projections): 64-row tiles, four blocks per CU
+      } else if (launch_dma<256, 160, 4, 1, 2, 2>(a, s)) {
       } else if (big) {
         launch_bf16<256, 160, 64, 4, 1>(a, s);
       } else {
