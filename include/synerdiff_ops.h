@@ -79,6 +79,18 @@ sd_status synerdiff_op_groupnorm_stats(int32_t dtype, const void* d_x0, int32_t 
 sd_status synerdiff_op_layernorm(int32_t dtype, const void* d_x, void* d_y, int64_t tokens, int32_t C,
                                  const float* d_gamma, const float* d_beta, float eps, void* hip_stream);
 
+/* Linear layer over a few fp32 rows, the per-request timestep-embedding
+ * MLP and time projections of the latent-diffusion UNet the paper serves
+ * (Sec. IV-A):
+ *   out[m, n] = act_out(bias[n] + add[m, n] + sum_k act_in(in[m, k]) * w[n, k])
+ * with act_* = SiLU where silu_* = 1, else the identity.  in [M, K] and out
+ * [M, N] fp32 (out must not overlap in; add may equal out), w [N, K] in
+ * `dtype`, bias [N] fp32; bias and add may be NULL.  K a multiple of 4;
+ * buffers 16-byte aligned.  M = 0 or N = 0 does nothing. */
+sd_status synerdiff_op_linear_rows(int32_t dtype, const float* d_in, int32_t M, int32_t K, const void* d_w,
+                                   const float* d_bias, const float* d_add, float* d_out, int32_t N,
+                                   int32_t silu_in, int32_t silu_out, void* hip_stream);
+
 /* GEGLU: y[t, j] = x[t, j] * GELU(x[t, half + j]) with exact GELU; x is
  * [tokens, 2*half], y [tokens, half]; half a multiple of 8. */
 sd_status synerdiff_op_geglu(int32_t dtype, const void* d_x, void* d_y, int64_t tokens, int32_t half,

@@ -77,11 +77,31 @@ hipError_t launch_time_inputs(const float* row_t, int rows, int temb_in, float* 
 }
 
 // ---------------------------------------------------------- small-M linear
-// out[m, n] = act_out(sum_k act_in(in[m, k]) W[n, k] + bias[n] + add[m, n]).
-// 64 columns per block; each thread owns one column and rows rg + 4 i.
-// Weights stream once; the input is staged in LDS 64 K-columns at a time.
+// out[m, n] = act_out(sum_k act_in(in[m, k]) W[n, k] + bias[n] + add[m, n])
+// for a few rows (the per-request time embedding: M = requests).  The
+// weights are the traffic: each wave owns 4 columns and streams their rows
+// with K spread over the lanes (lane l takes k = 4 l .. 4 l + 3 of each
+// 256-wide chunk), so every weight load is one contiguous run per column.
+// The input rows (32 per pass) are staged in LDS a chunk at a time and each
+// 16-byte read of them feeds 16 FMAs (4 columns x 4 k).  The 4 x 32 partial
+// dot products per lane are then summed across the wave by halving: six
+// exchange steps leave lane l with entries 2 l and 2 l + 1 (column l / 16,
+// rows 2 l % 32 and + 1), which it finishes and stores.
 namespace sm {
-constexpr int MMAX = 128, KC = 64;
+constexpr int MB = 32, KC = 256, CPW = 4, NWV = 4;
+}
+
+template <typename TW>
+__device__ inline void load4w(const TW* p, float w[4]);
+template <>
+__device__ inline void load4w<bf16>(const bf16* p, float w[4]) {
+  const bf16x4 v = *reinterpret_cast<const bf16x4*>(p);
+  w[0] = (float)v[0]; w[1] = (float)v[1]; w[2] = (float)v[2]; w[3] = (float)v[3];
+}
+template <>
+__device__ inline void load4w<float>(const float* p, float w[4]) {
+  const float4 v = *reinterpret_cast<const float4*>(p);
+  w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
 }
 
 template <typename TW>
@@ -90,49 +110,79 @@ __global__ __launch_bounds__(256) void linear_smallm_kernel(const float* in, int
                                                             float* out, int N, int silu_in,
                                                             int silu_out) {
   using namespace sm;
-  __shared__ float xs[MMAX][KC + 1];
-  const int tid = threadIdx.x, cn = tid & 63, rg = tid >> 6;
-  const int n = blockIdx.x * 64 + cn;
-  float acc[MMAX / 4];
+  __shared__ __attribute__((aligned(16))) float xs[MB][KC];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n0 = (blockIdx.x * NWV + wave) * CPW;  // the wave's first column
+  const int m0 = blockIdx.y * MB;
+  const int mrows = min(MB, M - m0);
+  float acc[CPW * MB];  // [column][row]
 #pragma unroll
-  for (int i = 0; i < MMAX / 4; ++i) acc[i] = 0.f;
+  for (int i = 0; i < CPW * MB; ++i) acc[i] = 0.f;
   for (int k0 = 0; k0 < K; k0 += KC) {
     __syncthreads();
-    for (int idx = tid; idx < M * KC; idx += 256) {
-      const int m = idx / KC, kk = idx - m * KC;
-      float v = (k0 + kk < K) ? in[(long)m * K + k0 + kk] : 0.f;
-      if (silu_in) v = silu_f(v);
-      xs[m][kk] = v;
+    for (int idx = tid; idx < MB * (KC / 4); idx += 256) {
+      const int m = idx / (KC / 4), kk = (idx - m * (KC / 4)) * 4;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (m < mrows && k0 + kk < K) {
+        v = *reinterpret_cast<const float4*>(in + (long)(m0 + m) * K + k0 + kk);
+        if (silu_in) {
+          v.x = silu_f(v.x); v.y = silu_f(v.y); v.z = silu_f(v.z); v.w = silu_f(v.w);
+        }
+      }
+      *reinterpret_cast<float4*>(&xs[m][kk]) = v;
     }
     __syncthreads();
-    if (n < N) {
-      for (int kk = 0; kk < KC; kk += 8) {
-        float w[8];
-        if (k0 + kk < K) {
-          load8f(W + (long)n * K + k0 + kk, w);
-        } else {
+    const int k = k0 + 4 * lane;
+    float w[CPW][4];
 #pragma unroll
-          for (int i = 0; i < 8; ++i) w[i] = 0.f;
-        }
+    for (int c = 0; c < CPW; ++c) {
+      if (k < K && n0 + c < N) {
+        load4w<TW>(W + (long)(n0 + c) * K + k, w[c]);
+      } else {
+        w[c][0] = w[c][1] = w[c][2] = w[c][3] = 0.f;
+      }
+    }
 #pragma unroll
-        for (int i = 0; i < MMAX / 4; ++i) {
-          const int m = rg + 4 * i;
-          if (m < M) {
+    for (int m = 0; m < MB; ++m) {
+      const float4 x = *reinterpret_cast<const float4*>(&xs[m][4 * lane]);
 #pragma unroll
-            for (int j = 0; j < 8; ++j) acc[i] = fmaf(xs[m][kk + j], w[j], acc[i]);
-          }
-        }
+      for (int c = 0; c < CPW; ++c) {
+        float t = acc[c * MB + m];
+        t = fmaf(x.x, w[c][0], t);
+        t = fmaf(x.y, w[c][1], t);
+        t = fmaf(x.z, w[c][2], t);
+        t = fmaf(x.w, w[c][3], t);
+        acc[c * MB + m] = t;
       }
     }
   }
+  // Sum over the wave by halving: at the step of lane bit b, a lane keeps
+  // the half of its live entries selected by that bit and adds its
+  // partner's copy of the same half.
+#pragma unroll
+  for (int st = 0; st < 6; ++st) {
+    const int h = (CPW * MB) >> (st + 1);  // entries kept after this step
+    const int off = 32 >> st;
+    const bool hi = (lane & off) != 0;
+#pragma unroll
+    for (int i = 0; i < CPW * MB / 2; ++i) {
+      if (i < h) {
+        const float keep = hi ? acc[i + h] : acc[i];
+        const float give = hi ? acc[i] : acc[i + h];
+        acc[i] = keep + __shfl_xor(give, off, 64);
+      }
+    }
+  }
+  // lane l now holds entries 2 l, 2 l + 1: column l / 16, rows 2 l % 32, + 1
+  const int n = n0 + lane / 16;
   if (n >= N) return;
 #pragma unroll
-  for (int i = 0; i < MMAX / 4; ++i) {
-    const int m = rg + 4 * i;
-    if (m < M) {
-      float v = acc[i] + (bias ? bias[n] : 0.f) + (add ? add[(long)m * N + n] : 0.f);
+  for (int e = 0; e < 2; ++e) {
+    const int m = (2 * lane) % MB + e;
+    if (m < mrows) {
+      float v = acc[e] + (bias ? bias[n] : 0.f) + (add ? add[(long)(m0 + m) * N + n] : 0.f);
       if (silu_out) v = silu_f(v);
-      out[(long)m * N + n] = v;
+      out[(long)(m0 + m) * N + n] = v;
     }
   }
 }
@@ -140,15 +190,15 @@ __global__ __launch_bounds__(256) void linear_smallm_kernel(const float* in, int
 hipError_t launch_linear_smallm(DType wdt, const float* in, int M, int K, const void* W,
                                 const float* bias, const float* add, float* out, int N,
                                 int silu_in, int silu_out, hipStream_t s) {
-  if (M <= 0) return hipSuccess;
-  if (M > sm::MMAX || K % 8) return hipErrorInvalidValue;
-  const unsigned blocks = (unsigned)((N + 63) / 64);
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (K <= 0 || K % 4) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)((N + sm::CPW * sm::NWV - 1) / (sm::CPW * sm::NWV)), (unsigned)((M + sm::MB - 1) / sm::MB));
   if (wdt == BF16)
-    linear_smallm_kernel<bf16><<<blocks, 256, 0, s>>>(in, M, K, (const bf16*)W, bias, add, out, N,
-                                                      silu_in, silu_out);
+    linear_smallm_kernel<bf16><<<grid, 256, 0, s>>>(in, M, K, (const bf16*)W, bias, add, out, N,
+                                                    silu_in, silu_out);
   else
-    linear_smallm_kernel<float><<<blocks, 256, 0, s>>>(in, M, K, (const float*)W, bias, add, out,
-                                                       N, silu_in, silu_out);
+    linear_smallm_kernel<float><<<grid, 256, 0, s>>>(in, M, K, (const float*)W, bias, add, out,
+                                                     N, silu_in, silu_out);
   return hipGetLastError();
 }
 

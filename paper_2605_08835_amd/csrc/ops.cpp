@@ -141,6 +141,21 @@ sd_status synerdiff_op_layernorm(int32_t dtype, const void* x, void* y, int64_t 
   return op_hip(launch_layernorm((DType)dtype, x, y, tokens, C, gamma, beta, eps, (hipStream_t)stream), "layernorm");
 }
 
+sd_status synerdiff_op_linear_rows(int32_t dtype, const float* in, int32_t M, int32_t K, const void* w,
+                                   const float* bias, const float* add, float* out, int32_t N, int32_t silu_in,
+                                   int32_t silu_out, void* stream) {
+  if (bad_dtype(dtype)) return op_fail(SD_ERR_INVALID_ARG, "bad dtype");
+  if (M < 0 || N < 0 || K <= 0 || K % 4) return op_fail(SD_ERR_INVALID_ARG, "bad shape");
+  if (M == 0 || N == 0) return SD_OK;
+  if (!in || !w || !out) return op_fail(SD_ERR_INVALID_ARG, "NULL argument");
+  const auto al = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
+  if (!al(in) || !al(w) || !al(out) || (bias && !al(bias)) || (add && !al(add)))
+    return op_fail(SD_ERR_INVALID_ARG, "buffers must be 16-byte aligned");
+  return op_hip(launch_linear_smallm((DType)dtype, in, M, K, w, bias, add, out, N, silu_in, silu_out,
+                                     (hipStream_t)stream),
+                "linear_rows");
+}
+
 sd_status synerdiff_op_geglu(int32_t dtype, const void* x, void* y, int64_t tokens, int32_t half, void* stream) {
   if (bad_dtype(dtype)) return op_fail(SD_ERR_INVALID_ARG, "bad dtype");
   if (!x || !y) return op_fail(SD_ERR_INVALID_ARG, "NULL argument");

@@ -60,6 +60,16 @@ def layernorm(x, gamma, beta, eps=1e-5):
     return y
 
 
+def linear_rows(x, w, bias=None, add=None, silu_in=0, silu_out=0):
+    """x fp32 [M, K], w [N, K] (fp32 or bf16) -> fp32 [M, N]."""
+    M, K = x.shape
+    N = w.shape[0]
+    y = torch.empty(M, N, device=x.device, dtype=torch.float32)
+    _check(lib().synerdiff_op_linear_rows(_dt(w), _ptr(x), M, K, _ptr(w), _ptr(bias), _ptr(add), _ptr(y), N,
+                                          int(silu_in), int(silu_out), _s()))
+    return y
+
+
 def geglu(x):
     half = x.shape[-1] // 2
     y = torch.empty(x.shape[:-1] + (half,), device=x.device, dtype=x.dtype)

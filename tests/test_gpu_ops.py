@@ -202,6 +202,52 @@ def test_layernorm(ops, dt, T, C):
     assert err <= (2e-6 if dt == "f32" else 6e-3), err
 
 
+def _silu(x):
+    return x / (1.0 + np.exp(-x))
+
+
+# M, K, N, weight dtype, silu_in, silu_out, bias, add: the time-embedding
+# shapes (320 -> 1280 -> 1280, SDXL's 2816 -> 1280, the stacked time
+# projections 1280 -> 20160) and ragged ones (K not a multiple of the
+# 256-wide chunk, N not a multiple of a block's 16 columns, M over 32).
+LINEAR_ROWS_CASES = [
+    (2, 32, 128, "f32", 0, 1, True, False),
+    (3, 36, 5, "f32", 1, 0, False, True),
+    (32, 320, 1280, "bf16", 0, 1, True, False),
+    (32, 1280, 1280, "bf16", 1, 0, True, True),
+    (33, 1280, 20160, "bf16", 1, 0, True, False),
+    (70, 2816, 1280, "bf16", 0, 1, True, False),
+    (1, 1000, 37, "bf16", 1, 1, False, False),
+    (0, 64, 16, "bf16", 0, 0, True, False),
+]
+
+
+@pytest.mark.parametrize("case", LINEAR_ROWS_CASES)
+def test_linear_rows(ops, case):
+    M, K, N, dt, si, so, with_bias, with_add = case
+    log(f"linear_rows {case}")
+    rng = np.random.default_rng(M * 7 + K + N)
+    x = rng.standard_normal((M, K)).astype(np.float32)
+    w = _vals(rng, (N, K), dt, 0.05)
+    b = (0.1 * rng.standard_normal(N)).astype(np.float32) if with_bias else None
+    add = rng.standard_normal((M, N)).astype(np.float32) if with_add else None
+    y = ops.linear_rows(_dev(x), _dev(w, dt), None if b is None else _dev(b), None if add is None else _dev(add),
+                        si, so)
+    torch.cuda.synchronize()
+    xd = x.astype(np.float64)
+    ref = (_silu(xd) if si else xd) @ w.astype(np.float64).T
+    if b is not None:
+        ref = ref + b
+    if add is not None:
+        ref = ref + add
+    if so:
+        ref = _silu(ref)
+    if M == 0:
+        assert y.shape == (0, N)
+        return
+    assert rel_l2(y.cpu().numpy(), ref) <= 2e-6
+
+
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 def test_geglu(ops, dt):
     log(f"geglu {dt}")
