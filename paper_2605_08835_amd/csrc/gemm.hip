@@ -117,8 +117,17 @@ __device__ inline void store4(const Epi& e, int m, int n, const float x[4]) {
   }
 }
 
+// Row scale (a folded LayerNorm's rstd); rows at or past M read nothing.
+__device__ inline float row_scale(const Epi& e, int m, int M) {
+  return (e.rowscale && m < M) ? e.rowscale[m] : 1.0f;
+}
+
 template <typename T>
 __device__ inline void epilogue4(const Epi& e, int m, int n, float x[4]) {
+  if (e.rowscale) {
+    const float rs = e.rowscale[m];
+    x[0] *= rs; x[1] *= rs; x[2] *= rs; x[3] *= rs;
+  }
   if (e.bias) {
     const float4 b = *reinterpret_cast<const float4*>(e.bias + n);
     x[0] += b.x; x[1] += b.y; x[2] += b.z; x[3] += b.w;
@@ -181,10 +190,11 @@ __device__ __forceinline__ void epilogue_tiles(const GemmArgs& a, const f32x16 (
             const int n = nt + 8 * q + hq;
             if (n < a.N) {
               float x[4], g[4];
+              const float rs = row_scale(a.epi, m, a.M);
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
-                x[e] = v[4 * q + e] + a.epi.bias[n + e];
-                g[e] = v[4 * (q + 2) + e] + a.epi.bias[n + 16 + e];
+                x[e] = fmaf(v[4 * q + e], rs, a.epi.bias[n + e]);
+                g[e] = fmaf(v[4 * (q + 2) + e], rs, a.epi.bias[n + 16 + e]);
                 x[e] *= gelu_as(g[e]);
               }
               store4<bf16>(a.epi, m, nt / 2 + 8 * q + hq, x);
@@ -198,6 +208,9 @@ __device__ __forceinline__ void epilogue_tiles(const GemmArgs& a, const f32x16 (
               float x[4] = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
               if (a.epi.vt_out && n >= a.epi.vt_col0) {
                 // transposed store: lanes l and l+1 hold consecutive tokens
+                const float rs = row_scale(a.epi, m, a.M);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) x[e] *= rs;
                 const int img = m / a.epi.vt_hw, tok = m - img * a.epi.vt_hw;
                 bf16* o = reinterpret_cast<bf16*>(a.epi.vt_out) + (long)img * a.epi.vt_img +
                           (long)(n - a.epi.vt_col0) * a.epi.vt_ld + tok;
@@ -255,6 +268,7 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 
       const f32x16 v = acc[I.value][J.value];
       const int nt = n0 + wn * WC + J.value * 32;
       const int m = mrow0 + lr;
+      const float rs = row_scale(e, m, a.M);
       if (geglu) {
         // packed columns 32t + u (a) and 32t + 16 + u (gate) -> channel 16t + u
 #pragma unroll
@@ -263,8 +277,8 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 
           float x[4];
 #pragma unroll
           for (int k = 0; k < 4; ++k) {
-            const float av = v[4 * q + k] + e.bias[n + k];
-            const float g = v[4 * (q + 2) + k] + e.bias[n + 16 + k];
+            const float av = fmaf(v[4 * q + k], rs, e.bias[n + k]);
+            const float g = fmaf(v[4 * (q + 2) + k], rs, e.bias[n + 16 + k]);
             x[k] = av * gelu_as(g);
           }
           bf16x4 o;
@@ -276,7 +290,7 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int n = nt + 8 * q + hq;
-          float x[4] = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+          float x[4] = {v[4 * q] * rs, v[4 * q + 1] * rs, v[4 * q + 2] * rs, v[4 * q + 3] * rs};
           if (e.bias) {
             const float4 b = *reinterpret_cast<const float4*>(e.bias + n);
             x[0] += b.x; x[1] += b.y; x[2] += b.z; x[3] += b.w;
@@ -328,12 +342,13 @@ __device__ __forceinline__ void epilogue_staged_vt(const GemmArgs& a, const f32x
   const int c0 = n0 + wn * WC - e.vt_col0;  // first V channel of the wave
   static_for<0, TM>([&](auto I) {
     const int mrow0 = m0 + wm * (BM / WM) + I.value * 32;
+    const float rs = row_scale(e, mrow0 + lr, a.M);
     static_for<0, TN>([&](auto J) {
       const f32x16 v = acc[I.value][J.value];
 #pragma unroll
       for (int q = 0; q < 4; ++q)
 #pragma unroll
-        for (int k = 0; k < 4; ++k) R[(J.value * 32 + 8 * q + hq + k) * 32 + lr] = (bf16)v[4 * q + k];
+        for (int k = 0; k < 4; ++k) R[(J.value * 32 + 8 * q + hq + k) * 32 + lr] = (bf16)(v[4 * q + k] * rs);
     });
     asm volatile("" ::: "memory");  // (one wave's LDS accesses complete in order)
     const int img = mrow0 / e.vt_hw, tok0 = mrow0 - img * e.vt_hw;
@@ -975,8 +990,9 @@ hipError_t launch_gemm(DType dt, const GemmArgs& args, hipStream_t s) {
                      a.epi.qcols % 4))
     return hipErrorInvalidValue;
   if (dt != BF16 && (a.epi.geglu || a.epi.vt_out)) return hipErrorInvalidValue;
-  if (a.epi.vt_out && (a.epi.vt_col0 % 8 || a.epi.resid || a.epi.bias || a.epi.tbias || a.epi.out_f32))
+  if (a.epi.vt_out && (a.epi.vt_col0 % 8 || a.epi.resid || a.epi.tbias || a.epi.out_f32))
     return hipErrorInvalidValue;
+  if (a.epi.rowscale && dt != BF16) return hipErrorInvalidValue;
   if ((long)a.N * a.ldb * (dt == BF16 ? 2 : 4) >= (1L << 31)) return hipErrorInvalidValue;
   if (dt == BF16) {
     auto nblk = [&](int bm, int bn) { return (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn); };

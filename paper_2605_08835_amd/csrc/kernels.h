@@ -42,12 +42,14 @@ struct Epi {
   int out_f32;            // 1: fp32 output regardless of the activation dtype
   int geglu;              // bf16 only: columns packed as 32-blocks [a(16) | gate(16)];
                           // out[m, 16t + u] = (a + b) * GELU(gate + b), ldo = N / 2
-  void* vt_out;           // bf16 only: columns n >= vt_col0 are written transposed,
+  void* vt_out;           // bf16 only: columns n >= vt_col0 are written transposed (no bias),
   int vt_col0, vt_hw;     //   vt_out[(m / vt_hw) * vt_img + (n - vt_col0) * vt_ld + m % vt_hw]
   int vt_ld;
   long vt_img;
   int qcols;              // columns n < qcols are multiplied by qscale before rounding
   float qscale;           //   (attention queries stored in base-2 logit units)
+  const float* rowscale;  // bf16 only: acc -> rowscale[m] * acc before the bias, or null (the
+                          //   LayerNorm rstd of input row m when the LN is folded into the weights)
 };
 
 struct GemmArgs {
@@ -96,6 +98,9 @@ hipError_t launch_groupnorm_apply(DType dt, const void* src0, int c0, const void
 
 hipError_t launch_layernorm(DType dt, const void* x, void* y, long tokens, int C, const float* gamma,
                             const float* beta, float eps, hipStream_t s);
+// Per-token LayerNorm scale: rstd[t] = 1 / sqrt(var_t + eps) (biased variance).
+hipError_t launch_layernorm_rstd(DType dt, const void* x, float* rstd, long tokens, int C, float eps,
+                                 hipStream_t s);
 
 // y[t, j] = x[t, j] * gelu(x[t, half + j]), j < half; x is [tokens, 2*half].
 hipError_t launch_geglu(DType dt, const void* x, void* y, long tokens, int half, hipStream_t s);

@@ -434,6 +434,54 @@ hipError_t launch_layernorm(DType dt, const void* x, void* y, long tokens, int C
   return hipGetLastError();
 }
 
+// The scale 1 / sqrt(var + eps) alone, for the projections that fold the
+// rest of the normalisation into their weights: one wave per token, two
+// passes over its registers as above.
+template <typename T>
+__global__ __launch_bounds__(256) void layernorm_rstd_kernel(const T* x, float* rstd, long tokens, int C,
+                                                             float eps) {
+  constexpr int MAXV = 4;
+  const long t = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= tokens) return;
+  const int CV = C / 8;
+  float v[MAXV][8];
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < MAXV; ++j) {
+    const int cv = lane + 64 * j;
+    if (cv < CV) {
+      load8f(x + t * C + cv * 8, v[j]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s += v[j][i];
+    }
+  }
+  const float mean = wave_sum(s) / C;
+  float q = 0.f;
+#pragma unroll
+  for (int j = 0; j < MAXV; ++j)
+    if (lane + 64 * j < CV)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float d = v[j][i] - mean;
+        q = fmaf(d, d, q);
+      }
+  const float r = rsqrtf(wave_sum(q) / C + eps);
+  if (lane == 0) rstd[t] = r;
+}
+
+hipError_t launch_layernorm_rstd(DType dt, const void* x, float* rstd, long tokens, int C, float eps,
+                                 hipStream_t s) {
+  if (tokens == 0) return hipSuccess;
+  if (C % 8 || C > 2048) return hipErrorInvalidValue;
+  const unsigned blocks = (unsigned)((tokens + 3) / 4);
+  if (dt == BF16)
+    layernorm_rstd_kernel<bf16><<<blocks, 256, 0, s>>>((const bf16*)x, rstd, tokens, C, eps);
+  else
+    layernorm_rstd_kernel<float><<<blocks, 256, 0, s>>>((const float*)x, rstd, tokens, C, eps);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ GEGLU
 template <typename T>
 __global__ void geglu_kernel(const T* x, T* y, long tokens, int half) {

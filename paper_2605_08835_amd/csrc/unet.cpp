@@ -34,18 +34,39 @@ static inline uint16_t f2bf(float f) {
   return (uint16_t)(u >> 16);
 }
 
+static inline float bf2f(uint16_t b) {
+  const uint32_t u = (uint32_t)b << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return f;
+}
+
 static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // ------------------------------------------------------------------ layout
 // P_*_GEGLU: rows of the GEGLU projection [a (4C) ; gate (4C)] reordered in
 // blocks of 32 as [a 16t..16t+15 | gate 16t..16t+15] so that one 32-column
 // MFMA tile holds matching value / gate columns.
-enum PackKind { P_ACT, P_F32, P_F32_SUM, P_CONV3, P_CONV3_SKIP, P_ACT_GEGLU, P_F32_GEGLU };
+// P_F32_VFOLD: self-attention output bias plus the output projection of the
+// value bias that a folded LayerNorm's shift gives V (names: out bias, out
+// weight, V weight, LN shift): b + W_o (W_v beta).  Attention rows of
+// probabilities sum to one, so a bias on V passes through to the output.
+enum PackKind { P_ACT, P_F32, P_F32_SUM, P_CONV3, P_CONV3_SKIP, P_ACT_GEGLU, P_F32_GEGLU, P_F32_VFOLD };
 struct PackJob {
   PackKind kind;
   size_t dst;
   std::vector<std::string> names;
   int cin_pad;
+  // P_ACT / P_ACT_GEGLU rows fed by a LayerNorm (bf16): each row becomes
+  // w' = gamma w - mean_k(gamma w), so that x . w' = (x - mean(x)) . (gamma w)
+  // for any input row x and the LN's mean subtraction happens inside the
+  // product; the job also writes the bias with beta's product added
+  // (fbias = bias + sum_k beta_k w_k; `bias` names the layer's bias, empty
+  // for none).  The rounding to bf16 carries each element's error into the
+  // next one, so a row's rounded elements still sum to ~0.
+  std::string lng, lnb, bias;
+  size_t fbias = 0;
+  bool qk_only = false;  // [Q; K; V] rows: only the Q rows keep their folded bias
 };
 
 struct ConvW {
@@ -61,6 +82,8 @@ struct ResW {
 };
 struct BlkW {
   size_t ln1g, ln1b, qkv, o1w, o1b, ln2g, ln2b, q2, kv2, o2w, o2b, ln3g, ln3b, f1w, f1b, f2w, f2b;
+  // bf16: folded biases of the LN-fed projections
+  size_t qkv_fb = 0, q2_fb = 0, f1_fb = 0;
 };
 struct TxW {
   int C = 0, heads = 0, d = 0;
@@ -77,7 +100,7 @@ struct LevelW {
 // Workspace roles (buffers sized by a dry run at max capacity).
 enum Role {
   R_X0, R_HA, R_HB, R_U, R_TZ, R_TX, R_TQ, R_TF, R_CTX, R_CKV, R_GNP, R_GNS, R_GNH,
-  R_E, R_A, R_H1, R_TAU, R_T2, R_TB, R_EPS, R_SCAL, R_GNA, R_TV, R_CVT, R_SPLIT, R_SKIP0
+  R_E, R_A, R_H1, R_TAU, R_T2, R_TB, R_EPS, R_SCAL, R_GNA, R_TV, R_CVT, R_SPLIT, R_LNS, R_SKIP0
 };
 
 }  // namespace sd
@@ -144,6 +167,16 @@ static size_t job_act(sd_unet* h, std::vector<std::string> names, size_t numel) 
   h->jobs.push_back(PackJob{P_ACT, d, std::move(names), 0});
   return d;
 }
+// Marks the last pack job as fed by LayerNorm `ln` (bf16 weights only) and
+// allocates its folded bias (rows fp32).
+static void fold_ln(sd_unet* h, const std::string& ln, size_t rows, const std::string& bias, size_t& fb) {
+  PackJob& j = h->jobs.back();
+  j.lng = ln + ".g";
+  j.lnb = ln + ".b";
+  j.bias = bias;
+  fb = j.fbias = walloc(h, rows * 4);
+}
+
 static size_t job_f32(sd_unet* h, std::vector<std::string> names, size_t numel, bool sum = false) {
   const size_t d = walloc(h, numel * 4);
   h->jobs.push_back(PackJob{sum ? P_F32_SUM : P_F32, d, std::move(names), 0});
@@ -206,11 +239,21 @@ static TxW transformer(sd_unet* h, const std::string& p, int C, int depth) {
     w.ln1g = job_f32(h, {b + ".ln1.g"}, C);
     w.ln1b = job_f32(h, {b + ".ln1.b"}, C);
     w.qkv = job_act(h, {b + ".attn1.q.w", b + ".attn1.k.w", b + ".attn1.v.w"}, 3 * CC);
+    if (h->dt == BF16) {
+      fold_ln(h, b + ".ln1", 3 * (size_t)C, "", w.qkv_fb);
+      h->jobs.back().qk_only = true;
+    }
     w.o1w = job_act(h, {b + ".attn1.o.w"}, CC);
-    w.o1b = job_f32(h, {b + ".attn1.o.b"}, C);
+    if (h->dt == BF16) {
+      w.o1b = walloc(h, (size_t)C * 4);
+      h->jobs.push_back(PackJob{P_F32_VFOLD, w.o1b, {b + ".attn1.o.b", b + ".attn1.o.w", b + ".attn1.v.w", b + ".ln1.b"}, 0});
+    } else {
+      w.o1b = job_f32(h, {b + ".attn1.o.b"}, C);
+    }
     w.ln2g = job_f32(h, {b + ".ln2.g"}, C);
     w.ln2b = job_f32(h, {b + ".ln2.b"}, C);
     w.q2 = job_act(h, {b + ".attn2.q.w"}, CC);
+    if (h->dt == BF16) fold_ln(h, b + ".ln2", C, "", w.q2_fb);
     w.kv2 = job_act(h, {b + ".attn2.k.w", b + ".attn2.v.w"}, (size_t)2 * C * c.ctx_dim);
     w.o2w = job_act(h, {b + ".attn2.o.w"}, CC);
     w.o2b = job_f32(h, {b + ".attn2.o.b"}, C);
@@ -219,6 +262,7 @@ static TxW transformer(sd_unet* h, const std::string& p, int C, int depth) {
     if (h->dt == BF16) {
       w.f1w = walloc(h, 8 * CC * h->esz);
       h->jobs.push_back(PackJob{P_ACT_GEGLU, w.f1w, {b + ".ff.w1"}, 0});
+      fold_ln(h, b + ".ln3", 8 * (size_t)C, b + ".ff.b1", w.f1_fb);
       w.f1b = walloc(h, 8 * (size_t)C * 4);
       h->jobs.push_back(PackJob{P_F32_GEGLU, w.f1b, {b + ".ff.b1"}, 0});
     } else {
@@ -509,8 +553,28 @@ struct Step {
     void* vbuf = h->dt == BF16 ? buf(R_TV, (size_t)T * C * h->esz) : nullptr;
     void* cvt = h->dt == BF16 ? buf(R_CVT, (size_t)(n_req + 1) * C * Lp * h->esz) : nullptr;
     gemm(lin(nh, C, T), nullptr, W(t.piw), C, epi(z, C, Wf(t.pib)), "proj_in", T);
+    // bf16: the three LayerNorms are folded into the projections they feed
+    // (mean subtraction and gain in the packed weights, shift in the bias,
+    // the per-token 1/std applied in the epilogue), so only that scale is
+    // computed here and the projections read z itself.  fp32: plain
+    // LayerNorm into x.
+    const bool fold = h->dt == BF16;
+    float* lns = fold ? (float*)buf(R_LNS, (size_t)T * 4) : nullptr;
+    auto layernorm = [&](size_t g, size_t bb, const char* name) -> const void* {
+      if (fold) {
+        if (!dry && !err) ok(launch_layernorm_rstd(h->dt, z, lns, T, C, 1e-5f, s), name, K_LN, 4.0 * T * C, (double)T * C * h->esz + 4.0 * T);
+        return z;
+      }
+      if (!dry && !err) ok(launch_layernorm(h->dt, z, x, T, C, Wf(g), Wf(bb), 1e-5f, s), name, K_LN, 8.0 * T * C, 2.0 * T * C * h->esz);
+      return x;
+    };
+    auto lnepi = [&](Epi& e, size_t fb) {
+      if (!fold) return;
+      e.rowscale = lns;
+      e.bias = Wf(fb);
+    };
     for (const BlkW& b : t.blk) {
-      if (!dry && !err) ok(launch_layernorm(h->dt, z, x, T, C, Wf(b.ln1g), Wf(b.ln1b), 1e-5f, s), "ln1", K_LN, 8.0 * T * C, 2.0 * T * C * h->esz);
+      const void* xin = layernorm(b.ln1g, b.ln1b, "ln1");
       // bf16: Q|K row-major [T, 2C], V transposed per image [rows][C][hw]
       // (the layout the attention kernel stages with 16-byte loads).
       const bool vt = h->dt == BF16;
@@ -527,7 +591,8 @@ struct Step {
         eq.vt_ld = hw;
         eq.vt_img = (long)C * hw;
       }
-      gemm(lin(x, C, T), nullptr, W(b.qkv), 3 * C, eq, "qkv", T);
+      lnepi(eq, b.qkv_fb);
+      gemm(lin(xin, C, T), nullptr, W(b.qkv), 3 * C, eq, "qkv", T);
       if (!dry && !err) {
         AttnArgs a;
         memset(&a, 0, sizeof(a));
@@ -550,14 +615,15 @@ struct Step {
            4.0 * T * C * h->esz);
       }
       gemm(lin(x, C, T), nullptr, W(b.o1w), C, epi(z, C, Wf(b.o1b), z, C), "attn1.out", T);
-      if (!dry && !err) ok(launch_layernorm(h->dt, z, x, T, C, Wf(b.ln2g), Wf(b.ln2b), 1e-5f, s), "ln2", K_LN, 8.0 * T * C, 2.0 * T * C * h->esz);
       {
+        const void* xin2 = layernorm(b.ln2g, b.ln2b, "ln2");
         Epi e2 = epi(q, C, nullptr);
         if (h->dt == BF16) {
           e2.qcols = C;
           e2.qscale = 1.4426950408889634f / sqrtf((float)t.d);
         }
-        gemm(lin(x, C, T), nullptr, W(b.q2), C, e2, "attn2.q", T);
+        lnepi(e2, b.q2_fb);
+        gemm(lin(xin2, C, T), nullptr, W(b.q2), C, e2, "attn2.q", T);
       }
       {
         const bool vt = h->dt == BF16;
@@ -593,13 +659,14 @@ struct Step {
         }
       }
       gemm(lin(x, C, T), nullptr, W(b.o2w), C, epi(z, C, Wf(b.o2b), z, C), "attn2.out", T);
-      if (!dry && !err) ok(launch_layernorm(h->dt, z, x, T, C, Wf(b.ln3g), Wf(b.ln3b), 1e-5f, s), "ln3", K_LN, 8.0 * T * C, 2.0 * T * C * h->esz);
+      const void* xin3 = layernorm(b.ln3g, b.ln3b, "ln3");
       if (h->dt == BF16) {  // GEGLU fused into the projection's epilogue
         Epi ef = epi(q, 4 * C, Wf(b.f1b));
         ef.geglu = 1;
-        gemm(lin(x, C, T), nullptr, W(b.f1w), 8 * C, ef, "ff1+geglu", T);
+        lnepi(ef, b.f1_fb);
+        gemm(lin(xin3, C, T), nullptr, W(b.f1w), 8 * C, ef, "ff1+geglu", T);
       } else {
-        gemm(lin(x, C, T), nullptr, W(b.f1w), 8 * C, epi(f, 8 * C, Wf(b.f1b)), "ff1", T);
+        gemm(lin(xin3, C, T), nullptr, W(b.f1w), 8 * C, epi(f, 8 * C, Wf(b.f1b)), "ff1", T);
         if (!dry && !err)
           ok(launch_geglu(h->dt, f, q, T, 4 * C, s), "geglu", K_GEGLU, 4.0 * T * 4 * C, 12.0 * T * C * h->esz);
       }
@@ -912,6 +979,62 @@ sd_status synerdiff_load_weights(sd_unet* h, const float* hp, size_t n_floats, v
       if (it == by.end()) return fail(SD_ERR_INVALID_ARG, "internal: missing parameter " + n);
       src.push_back(it->second);
     }
+    if (!j.lng.empty()) {
+      // LayerNorm-fed projection: source rows in packed order (GEGLU rows
+      // reordered as below), each folded with the LN gain and shift.
+      auto find = [&](const std::string& n) -> const Param* {
+        auto it = by.find(n);
+        return it == by.end() ? nullptr : it->second;
+      };
+      const Param* g = find(j.lng);
+      const Param* be = find(j.lnb);
+      const Param* bi = j.bias.empty() ? nullptr : find(j.bias);
+      if (!g || !be || (!j.bias.empty() && !bi)) return fail(SD_ERR_INVALID_ARG, "internal: missing LN parameter");
+      const size_t K = g->numel;
+      std::vector<const float*> rowsrc;
+      std::vector<float> rowbias;
+      for (auto* p : src)
+        for (size_t r = 0; r < p->numel / K; ++r) rowsrc.push_back(hp + p->offset + r * K);
+      rowbias.assign(rowsrc.size(), 0.f);
+      if (bi)
+        for (size_t r = 0; r < rowsrc.size(); ++r) rowbias[r] = hp[bi->offset + r];
+      if (j.kind == P_ACT_GEGLU) {
+        const size_t rows8 = rowsrc.size(), half = rows8 / 2;
+        std::vector<const float*> rs(rows8);
+        std::vector<float> rb(rows8);
+        for (size_t r = 0; r < rows8; ++r) {
+          const size_t t = r / 32, u = r % 32;
+          const size_t srow = u < 16 ? 16 * t + u : half + 16 * t + (u - 16);
+          rs[r] = rowsrc[srow];
+          rb[r] = rowbias[srow];
+        }
+        rowsrc.swap(rs);
+        rowbias.swap(rb);
+      }
+      const float* gam = hp + g->offset;
+      const float* bet = hp + be->offset;
+      for (size_t r = 0; r < rowsrc.size(); ++r) {
+        double mean = 0.0, fb = rowbias[r];
+        for (size_t k = 0; k < K; ++k) {
+          mean += (double)gam[k] * rowsrc[r][k];
+          fb += (double)bet[k] * rowsrc[r][k];
+        }
+        mean /= (double)K;
+        double carry = 0.0;  // rounding error carried to the next element
+        for (size_t k = 0; k < K; ++k) {
+          const double want = (double)gam[k] * rowsrc[r][k] - mean + carry;
+          const float w = bf ? bf2f(f2bf((float)want)) : (float)want;
+          put_act(j.dst, r * K + k, w);
+          carry = want - (double)w;
+        }
+        // self-attention projections: keys need no bias (a shift of every
+        // score of a query by the same q . b cancels in the softmax) and the
+        // value bias moves to the output projection's bias (P_F32_VFOLD)
+        const float fbf = (j.qk_only && r >= K) ? 0.f : (float)fb;
+        memcpy(&host[j.fbias + r * 4], &fbf, 4);
+      }
+      continue;
+    }
     switch (j.kind) {
       case P_ACT: {
         size_t o = 0;
@@ -941,6 +1064,19 @@ sd_status synerdiff_load_weights(sd_unet* h, const float* hp, size_t n_floats, v
             else
               memcpy(&host[j.dst + (r * cols + k) * 4], &v, 4);
           }
+        }
+        break;
+      }
+      case P_F32_VFOLD: {
+        const size_t C = src[0]->numel;
+        std::vector<double> vb(C, 0.0);
+        for (size_t c = 0; c < C; ++c)
+          for (size_t k = 0; k < C; ++k) vb[c] += (double)hp[src[3]->offset + k] * hp[src[2]->offset + c * C + k];
+        for (size_t n = 0; n < C; ++n) {
+          double v = hp[src[0]->offset + n];
+          for (size_t c = 0; c < C; ++c) v += (double)hp[src[1]->offset + n * C + c] * vb[c];
+          const float f = (float)v;
+          memcpy(&host[j.dst + n * 4], &f, 4);
         }
         break;
       }
