@@ -35,10 +35,11 @@ hipError_t launch_pack_latents(DType dt, const float* lat, void* x0, int rows, i
 
 // ------------------------------------------------------ time-embedding inputs
 // Sinusoid [cos(t f_i) | sin(t f_i)], f_i = 10000^(-i/half), evaluated in
-// fp64 so the argument t f_i (up to ~1e3 rad) keeps full fp32 accuracy.
-__device__ inline void sinusoid(double t, int dim, float* out) {
+// fp64 so the argument t f_i (up to ~1e3 rad) keeps full fp32 accuracy;
+// thread `part` of `parts` takes i = part, part + parts, ...
+__device__ inline void sinusoid(double t, int dim, float* out, int part = 0, int parts = 1) {
   const int half = dim / 2;
-  for (int i = 0; i < half; ++i) {
+  for (int i = part; i < half; i += parts) {
     const double f = exp(-9.210340371976184 * (double)i / (double)half);  // ln(1e4)
     double sv, cv;
     sincos(t * f, &sv, &cv);
@@ -53,14 +54,14 @@ __global__ void time_inputs_kernel(const float* row_t, int rows, int temb_in, fl
                                    const float* time_ids, int n_ids, int id_dim, float* a) {
   const int row = blockIdx.x;
   if (row >= rows) return;
-  if (threadIdx.x == 0) sinusoid((double)row_t[row], temb_in, e + (long)row * temb_in);
+  sinusoid((double)row_t[row], temb_in, e + (long)row * temb_in, threadIdx.x, blockDim.x);
   if (a) {
     const int add_in = pooled_dim + n_ids * id_dim;
     float* ar = a + (long)row * add_in;
     const float* pooled = row_branch[row] ? pooled_uncond : pooled_cond + (long)row_req[row] * pooled_dim;
     for (int i = threadIdx.x; i < pooled_dim; i += blockDim.x) ar[i] = pooled[i];
-    if (threadIdx.x < n_ids)
-      sinusoid((double)time_ids[threadIdx.x], id_dim, ar + pooled_dim + threadIdx.x * id_dim);
+    for (int id = 0; id < n_ids; ++id)
+      sinusoid((double)time_ids[id], id_dim, ar + pooled_dim + id * id_dim, threadIdx.x, blockDim.x);
   }
 }
 
@@ -79,16 +80,17 @@ hipError_t launch_time_inputs(const float* row_t, int rows, int temb_in, float* 
 // ---------------------------------------------------------- small-M linear
 // out[m, n] = act_out(sum_k act_in(in[m, k]) W[n, k] + bias[n] + add[m, n])
 // for a few rows (the per-request time embedding: M = requests).  The
-// weights are the traffic: each wave owns 4 columns and streams their rows
+// weights are the traffic: each wave owns 2 columns and streams their rows
 // with K spread over the lanes (lane l takes k = 4 l .. 4 l + 3 of each
 // 256-wide chunk), so every weight load is one contiguous run per column.
-// The input rows (32 per pass) are staged in LDS a chunk at a time and each
-// 16-byte read of them feeds 16 FMAs (4 columns x 4 k).  The 4 x 32 partial
-// dot products per lane are then summed across the wave by halving: six
-// exchange steps leave lane l with entries 2 l and 2 l + 1 (column l / 16,
-// rows 2 l % 32 and + 1), which it finishes and stores.
+// The input rows (64 per pass, so a step's rows usually take one pass over
+// the weights) are staged in LDS a chunk at a time and each 16-byte read of
+// them feeds 8 FMAs (2 columns x 4 k).  The 2 x 64 partial dot products per
+// lane are then summed across the wave by halving: six exchange steps leave
+// lane l with entries 2 l and 2 l + 1 (column l / 32, rows 2 l % 64 and
+// + 1), which it finishes and stores.
 namespace sm {
-constexpr int MB = 32, KC = 256, CPW = 4, NWV = 4;
+constexpr int MB = 64, KC = 256, CPW = 2, NWV = 4;  // CPW * MB = 128 partial sums per lane
 }
 
 template <typename TW>
@@ -173,8 +175,9 @@ __global__ __launch_bounds__(256) void linear_smallm_kernel(const float* in, int
       }
     }
   }
-  // lane l now holds entries 2 l, 2 l + 1: column l / 16, rows 2 l % 32, + 1
-  const int n = n0 + lane / 16;
+  // lane l now holds entries 2 l, 2 l + 1: column 2 l / MB, rows 2 l % MB, + 1
+  static_assert(CPW * MB == 128, "the halving leaves two entries per lane");
+  const int n = n0 + 2 * lane / MB;
   if (n >= N) return;
 #pragma unroll
   for (int e = 0; e < 2; ++e) {
