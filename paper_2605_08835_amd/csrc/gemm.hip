@@ -588,7 +588,7 @@ __device__ __forceinline__ int swz(int r) {
   return CPR == 4 ? (r >> 2) & 3 : (r >> 1) & 7;
 }
 
-template <int BM, int BN, int WM, int WN, int MODE, int DNS, int MINB, int DK>
+template <int BM, int BN, int WM, int WN, int MODE, int DNS, int MINB, int DK, bool TI>
 __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmArgs a) {
   constexpr int NWV = WM * WN;                          // waves per block
   constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
@@ -657,6 +657,13 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
   const int nk_all = (a.K + DK - 1) / DK;  // K is a multiple of DK in modes 1, 2
   const int per = (nk_all + a.ksplit - 1) / a.ksplit;
   const int kb = split * per, ke = min(nk_all, kb + per);
+  // With TI (images larger than 8x8) the K tiles are visited channel block
+  // by channel block, all taps of a block in a row (the packed weights stay
+  // tap-major: a tile's weight columns follow from its tap and channel
+  // block), so consecutive tiles read the same input rows shifted by a tap
+  // and find them in L1 / L2; smaller images (a 256-row tile spans several)
+  // go tap by tap.  The order is a property of the layer, like the split.
+  constexpr bool tapin = TI;
   int st_seg = 0, st_tap = 0, st_cb = 0;
   {  // loader state at K tile kb
     int kk = kb * DK;
@@ -664,25 +671,43 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
       st_seg = 1;
       kk -= a.seg[0].K;
     }
-    const int gcin = st_seg ? a.seg[1].cin : a.seg[0].cin;
-    st_tap = kk / gcin;
-    st_cb = kk - st_tap * gcin;
+    const int gks = st_seg ? a.seg[1].ks : a.seg[0].ks, gcin = st_seg ? a.seg[1].cin : a.seg[0].cin;
+    const int i = kk / DK, taps = gks * gks;
+    if constexpr (tapin) {
+      st_cb = (i / taps) * DK;
+      st_tap = i - (i / taps) * taps;
+    } else {
+      st_tap = kk / gcin;
+      st_cb = kk - st_tap * gcin;
+    }
   }
   // Issue the loads of K tile kt into stage `stg` (tiles are issued in order).
   auto issue = [&](int kt, int stg) {
-    const int k0 = kt * DK;
+    (void)kt;
     const bool s1 = MODE == 1 && st_seg;
     const int gcin = s1 ? a.seg[1].cin : a.seg[0].cin, gks = s1 ? a.seg[1].ks : a.seg[0].ks;
     const int gc0 = s1 ? a.seg[1].c0 : a.seg[0].c0, gc1 = s1 ? a.seg[1].c1 : a.seg[0].c1;
     const void* gs0 = s1 ? a.seg[1].src0 : a.seg[0].src0;
     const void* gs1 = s1 ? a.seg[1].src1 : a.seg[0].src1;
     const int tap = st_tap, cb = st_cb;
-    st_cb += DK;
-    if (st_cb >= gcin) {
-      st_cb = 0;
+    const int k0 = (s1 ? a.seg[0].K : 0) + tap * gcin + cb;  // the tile's weight columns
+    if constexpr (tapin) {
       if (++st_tap == gks * gks) {
         st_tap = 0;
-        st_seg = 1;
+        st_cb += DK;
+        if (st_cb >= gcin) {
+          st_cb = 0;
+          st_seg = 1;
+        }
+      }
+    } else {
+      st_cb += DK;
+      if (st_cb >= gcin) {
+        st_cb = 0;
+        if (++st_tap == gks * gks) {
+          st_tap = 0;
+          st_seg = 1;
+        }
       }
     }
     const bool in0 = cb < gc0;
@@ -949,10 +974,17 @@ static bool launch_dma(const GemmArgs& a, hipStream_t s) {
   if (mode == 0 || (DK != DKS && a.ksplit > 1)) return false;
   const long blocks = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN) * a.ksplit;
   const dim3 g((unsigned)blocks), b(64 * WM * WN);
-  if (mode == 1)
-    gemm_bf16_dma_kernel<BM, BN, WM, WN, 1, DNS, MINB, DK><<<g, b, 0, s>>>(a);
+  // K order (see the kernel): channel block outer, taps inner on images
+  // larger than 8x8.
+  const bool ti = (long)a.seg[0].Ho * a.seg[0].Wo > 64;
+  if (mode == 1 && ti)
+    gemm_bf16_dma_kernel<BM, BN, WM, WN, 1, DNS, MINB, DK, true><<<g, b, 0, s>>>(a);
+  else if (mode == 1)
+    gemm_bf16_dma_kernel<BM, BN, WM, WN, 1, DNS, MINB, DK, false><<<g, b, 0, s>>>(a);
+  else if (ti)
+    gemm_bf16_dma_kernel<BM, BN, WM, WN, 2, DNS, MINB, DK, true><<<g, b, 0, s>>>(a);
   else
-    gemm_bf16_dma_kernel<BM, BN, WM, WN, 2, DNS, MINB, DK><<<g, b, 0, s>>>(a);
+    gemm_bf16_dma_kernel<BM, BN, WM, WN, 2, DNS, MINB, DK, false><<<g, b, 0, s>>>(a);
   if (a.ksplit > 1) {
     const long n = (long)a.M * (a.N / 4);
     splitk_reduce_kernel<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s>>>(a);
