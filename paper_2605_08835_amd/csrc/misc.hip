@@ -80,17 +80,16 @@ hipError_t launch_time_inputs(const float* row_t, int rows, int temb_in, float* 
 // ---------------------------------------------------------- small-M linear
 // out[m, n] = act_out(sum_k act_in(in[m, k]) W[n, k] + bias[n] + add[m, n])
 // for a few rows (the per-request time embedding: M = requests).  The
-// weights are the traffic: each wave owns 2 columns and streams their rows
+// weights are the traffic: each wave owns 4 columns and streams their rows
 // with K spread over the lanes (lane l takes k = 4 l .. 4 l + 3 of each
 // 256-wide chunk), so every weight load is one contiguous run per column.
-// The input rows (64 per pass, so a step's rows usually take one pass over
-// the weights) are staged in LDS a chunk at a time and each 16-byte read of
-// them feeds 8 FMAs (2 columns x 4 k).  The 2 x 64 partial dot products per
-// lane are then summed across the wave by halving: six exchange steps leave
-// lane l with entries 2 l and 2 l + 1 (column l / 32, rows 2 l % 64 and
-// + 1), which it finishes and stores.
+// The input rows (32 per pass) are staged in LDS a chunk at a time and each
+// 16-byte read of them feeds 16 FMAs (4 columns x 4 k).  The 4 x 32 partial
+// dot products per lane are then summed across the wave by halving: six
+// exchange steps leave lane l with entries 2 l and 2 l + 1 (column l / 16,
+// rows 2 l % 32 and + 1), which it finishes and stores.
 namespace sm {
-constexpr int MB = 64, KC = 256, CPW = 2, NWV = 4;  // CPW * MB = 128 partial sums per lane
+constexpr int MB = 32, KC = 256, CPW = 4, NWV = 4;  // CPW * MB = 128 partial sums per lane
 }
 
 template <typename TW>
