@@ -45,16 +45,16 @@ __device__ inline float silu_f(float x) { return x / (1.0f + __expf(-x)); }
 // bf16 rounding): for u >= 0, 1 - erf(u) = t (a1 + t (a2 + t (a3 + t (a4 +
 // t a5)))) exp(-u^2), t = 1 / (1 + p u).  A reciprocal and an exp2 are its
 // only transcendental instructions, against a library erff's piecewise
-// polynomials; the bf16 GEGLU epilogues use it.
+// polynomials; the bf16 GEGLU epilogues use it.  The 1/sqrt(2) of u and
+// the 1/2 of h are folded into the constants (p / sqrt 2, a_i / 2).
 __device__ inline float gelu_as(float x) {
-  const float u = fabsf(x) * 0.70710678118654752f;
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, u, 1.0f));
-  float p = fmaf(t, 1.061405429f, -1.453152027f);
-  p = fmaf(t, p, 1.421413741f);
-  p = fmaf(t, p, -0.284496736f);
-  p = fmaf(t, p, 0.254829592f);
-  // h = (1 - erf(u)) / 2; exp(-u^2) = exp2(-x^2 log2(e) / 2)
-  const float h = 0.5f * t * p * __builtin_amdgcn_exp2f(x * x * -0.72134752044448170f);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.23164193223f, fabsf(x), 1.0f));  // 1 / (1 + p u)
+  float p = fmaf(t, 0.5307027145f, -0.7265760135f);
+  p = fmaf(t, p, 0.7107068705f);
+  p = fmaf(t, p, -0.142248368f);
+  p = fmaf(t, p, 0.127414796f);
+  // h = (1 - erf(u)) / 2 = t p exp(-u^2) with the halved a_i; exp(-u^2) = exp2(-x^2 log2(e) / 2)
+  const float h = t * p * __builtin_amdgcn_exp2f(x * x * -0.72134752044448170f);
   return x * (x >= 0.f ? 1.0f - h : h);
 }
 
