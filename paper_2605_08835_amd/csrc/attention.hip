@@ -213,8 +213,15 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
   for (int g = 0; g < QG; ++g) m_run[g] = l_run[g] = 0.f;
   const bool vvec = (a.v_ld & 7) == 0;
 
-  bf16x8 rk[KPT], rv[VPT];
-  auto fetch = [&](int k0) {
+  // PF2 (the narrow heads with the max in the product, d = 40 for SD):
+  // two register sets, the tile after next fetched while this one is
+  // computed and the next one (fetched a tile earlier) staged into LDS, so a
+  // fetch has two tiles of time to land (measured +4 % at d = 40; at the
+  // wider heads it measured slower or ran out of registers).  Otherwise the
+  // next tile is fetched during this one, into the single set it needs.
+  constexpr bool PF2 = QG == 2 && D16 == 48 && MF;
+  bf16x8 rk0[KPT], rv0[VPT], rk1[KPT], rv1[VPT];
+  auto fetch = [&](int k0, bf16x8 (&rk)[KPT], bf16x8 (&rv)[VPT]) {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int idx = tid + NT * i;
@@ -251,7 +258,7 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
       rv[i] = v;
     }
   };
-  auto stage = [&](int b) {
+  auto stage = [&](int b, const bf16x8 (&rk)[KPT], const bf16x8 (&rv)[VPT]) {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int idx = tid + NT * i;
@@ -266,16 +273,24 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
     }
   };
 
-  fetch(0);
-  stage(0);
+  fetch(0, rk0, rv0);
+  stage(0, rk0, rv0);
+  if (PF2 && KT < a.Nk) fetch(KT, rk1, rv1);
   __syncthreads();
   // One 64-key tile; the last tile, if partial, is a separate instance so
   // the full tiles carry no masking code.
-  auto tile = [&](auto tl, int k0, int it) {
+  // fk / fv: the set to fetch the tile after next into; sk / sv: the set
+  // holding the next tile, staged at the end.
+  auto tile = [&](auto tl, int k0, int it, bf16x8 (&fk)[KPT], bf16x8 (&fv)[VPT], bf16x8 (&sk)[KPT],
+                  bf16x8 (&sv)[VPT]) {
     constexpr bool TAIL = decltype(tl)::value;
     const int b = it & 1;
     const bool more = k0 + KT < a.Nk;
-    if (more) fetch(k0 + KT);
+    if constexpr (PF2) {
+      if (k0 + 2 * KT < a.Nk) fetch(k0 + 2 * KT, fk, fv);
+    } else {
+      if (more) fetch(k0 + KT, sk, sv);
+    }
     const bf16* Kb = Ks[b];
     const bf16* Vb = Vt[b];
 
@@ -320,12 +335,25 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
         for (int g = 0; g < QG; ++g) o[g][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[g], o[g][t], 0, 0, 0);
       }
     }
-    if (more) stage(b ^ 1);
+    if (more) stage(b ^ 1, sk, sv);
     __syncthreads();
   };
   const int nfull = a.Nk / KT;
-  for (int it = 0; it < nfull; ++it) tile(BC<false>{}, it * KT, it);
-  if (nfull * KT < a.Nk) tile(BC<true>{}, nfull * KT, nfull);
+  int it = 0;
+  if constexpr (PF2) {
+    for (; it + 1 < nfull; it += 2) {
+      tile(BC<false>{}, it * KT, it, rk0, rv0, rk1, rv1);
+      tile(BC<false>{}, (it + 1) * KT, it + 1, rk1, rv1, rk0, rv0);
+    }
+    if (it < nfull) {
+      tile(BC<false>{}, it * KT, it, rk0, rv0, rk1, rv1);
+      ++it;
+    }
+  } else {
+    for (; it < nfull; ++it) tile(BC<false>{}, it * KT, it, rk0, rv0, rk0, rv0);
+  }
+  // (the partial last tile fetches and stages nothing)
+  if (nfull * KT < a.Nk) tile(BC<true>{}, nfull * KT, it, rk0, rv0, rk1, rv1);
 
   // O^T accumulator: lane holds head dims t*32 + 8(r/4) + 4 lh + [0, 4) of
   // its query; each run of 4 is one 8-byte store.
