@@ -45,6 +45,19 @@ sd_status synerdiff_op_conv(int32_t dtype, const void* d_x0, int32_t c0, const v
 int64_t synerdiff_op_conv_scratch_floats(int32_t dtype, int32_t c0, int32_t c1, int32_t n, int32_t H, int32_t W,
                                          int32_t ks, int32_t stride, int32_t up, int32_t cout);
 
+/* The 3x3 convolution (zero padding 1) of a nearest-2x upsampled input, as
+ * the bf16 step runs the UNet's upsampling layers: four 2x2 convolutions on
+ * the input grid, one per output phase.  Output pixel (2y + py, 2x + px)
+ * = bias + sum over taps (ty, tx) in {0,1}^2 and channels c of
+ * x[y + py - 1 + ty, x + px - 1 + tx, c] (zero outside) * w[2 py + px, o, 2 ty + tx, c],
+ * where phase weight (ty, tx) is the sum of the 3x3 taps (ky, kx) with
+ * floor((py + ky - 1) / 2) = py - 1 + ty and floor((px + kx - 1) / 2) =
+ * px - 1 + tx.  x [n, H, W, cin] and out [n, 2H, 2W, cout] bf16, w bf16
+ * [4][cout][4 cin], bias fp32 [cout] or NULL.  dtype must be SD_BF16;
+ * cin a multiple of 32, cout of 160 (else SD_ERR_INVALID_ARG). */
+sd_status synerdiff_op_upconv(int32_t dtype, const void* d_x, int32_t n, int32_t H, int32_t W, int32_t cin,
+                              const void* d_w, int32_t cout, const float* d_bias, void* d_out, void* hip_stream);
+
 /* Multi-head attention O = softmax(Q K^T * scale) V per image and head
  * (head h uses channels [h*d, (h+1)*d)).  Q: image i, token t, channel c at
  * q + i*q_img + t*q_ld + c; K likewise with k_img, k_ld and image

@@ -81,6 +81,8 @@ _SIG = {
     "synerdiff_op_layernorm": (ctypes.c_int, [ctypes.c_int32, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P,
                                               ctypes.c_float, _P]),
     "synerdiff_op_geglu": (ctypes.c_int, [ctypes.c_int32, _P, _P, ctypes.c_int64, ctypes.c_int32, _P]),
+    "synerdiff_op_upconv": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                           ctypes.c_int32, _P, ctypes.c_int32, _P, _P, _P]),
     "synerdiff_op_linear_rows": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P,
                                                 ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P]),
 }

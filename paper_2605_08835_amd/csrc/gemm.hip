@@ -103,17 +103,27 @@ __device__ inline void epilogue_store(const Epi& e, int row, int col, float v) {
     reinterpret_cast<T*>(e.out)[(long)row * e.ldo + col] = from_f<T>(v);
 }
 
+// Output row of GEMM row m (the upsample phases write every other pixel of
+// every other image row).
+__device__ inline long out_row(const Epi& e, int m) {
+  if (!e.phase) return m;
+  const int hw = e.ph_h * e.ph_w, img = m / hw, p = m - img * hw, y = p / e.ph_w, x = p - y * e.ph_w;
+  const int py = (e.phase - 1) >> 1, px = (e.phase - 1) & 1;
+  return (long)img * 4 * hw + (long)(2 * y + py) * (2 * e.ph_w) + 2 * x + px;
+}
+
 // Four consecutive output channels n..n+3 of row m (n % 4 == 0, N % 4 == 0).
 template <typename T>
 __device__ inline void store4(const Epi& e, int m, int n, const float x[4]) {
+  const long r = out_row(e, m);
   if (e.out_f32) {
-    *reinterpret_cast<float4*>(reinterpret_cast<float*>(e.out) + (long)m * e.ldo + n) =
+    *reinterpret_cast<float4*>(reinterpret_cast<float*>(e.out) + r * e.ldo + n) =
         make_float4(x[0], x[1], x[2], x[3]);
   } else {
     bf16x4 o;
 #pragma unroll
     for (int i = 0; i < 4; ++i) o[i] = (bf16)x[i];
-    *reinterpret_cast<bf16x4*>(reinterpret_cast<T*>(e.out) + (long)m * e.ldo + n) = o;
+    *reinterpret_cast<bf16x4*>(reinterpret_cast<T*>(e.out) + r * e.ldo + n) = o;
   }
 }
 
@@ -321,7 +331,7 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 
       const int row = c / cpr, ch = c - row * cpr;
       const int m = mrow0 + row;
       if (m < a.M && ncol0 + ch * 8 < (geglu ? a.N / 2 : a.N))
-        *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(e.out) + (long)m * e.ldo + ncol0 + ch * 8) =
+        *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(e.out) + out_row(e, m) * e.ldo + ncol0 + ch * 8) =
             *reinterpret_cast<const bf16x8*>(R + row * LD + ch * 8);
     }
     asm volatile("" ::: "memory");
@@ -464,8 +474,13 @@ __global__ __launch_bounds__(256, MINB) void gemm_bf16_kernel(GemmArgs a) {
       if constexpr (MODE == 1) {
         const long npix = a.M;
         const __amdgpu_buffer_rsrc_t ares = make_rsrc(in0 ? gs0 : gs1, npix * cs * 2);
-        const int t9 = gks == 3 ? tap : 4;  // a 1x1 tap is the centre of the 3x3 mask
-        const int dpix = gks == 3 ? (tap / 3 - 1) * Wo + (tap % 3 - 1) : 0;
+        // tap offset (dy, dx) and its bit in the 3x3 in-image mask (a 1x1 tap
+        // is the centre; an upsample phase's 2x2 taps are four of the nine)
+        const int gpy = s1 ? a.seg[1].py : a.seg[0].py, gpx = s1 ? a.seg[1].px : a.seg[0].px;
+        const int tdy = gks == 3 ? tap / 3 - 1 : (gks == 2 ? gpy - 1 + (tap >> 1) : 0);
+        const int tdx = gks == 3 ? tap % 3 - 1 : (gks == 2 ? gpx - 1 + (tap & 1) : 0);
+        const int t9 = (tdy + 1) * 3 + tdx + 1;
+        const int dpix = tdy * Wo + tdx;
 #pragma unroll
         for (int j = 0; j < AR; ++j) {
           const bool ok = live && ((ra1[j] >> t9) & 1);
@@ -715,8 +730,13 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
     bf16* adst = As + stg * BM * DK;
     if constexpr (MODE == 1) {
       const __amdgpu_buffer_rsrc_t ares = make_rsrc(in0 ? gs0 : gs1, (long)a.M * cs * 2);
-      const int t9 = gks == 3 ? tap : 4;
-      const int dpix = gks == 3 ? (tap / 3 - 1) * Wo + (tap % 3 - 1) : 0;
+      // tap offset (dy, dx) and its bit in the 3x3 in-image mask (a 1x1 tap
+      // is the centre; an upsample phase's 2x2 taps are four of the nine)
+      const int gpy = s1 ? a.seg[1].py : a.seg[0].py, gpx = s1 ? a.seg[1].px : a.seg[0].px;
+      const int tdy = gks == 3 ? tap / 3 - 1 : (gks == 2 ? gpy - 1 + (tap >> 1) : 0);
+      const int tdx = gks == 3 ? tap % 3 - 1 : (gks == 2 ? gpx - 1 + (tap & 1) : 0);
+      const int t9 = (tdy + 1) * 3 + tdx + 1;
+      const int dpix = tdy * Wo + tdx;
 #pragma unroll
       for (int j = 0; j < AW; ++j) {
         const bool ok = (ra1[j] >> t9) & 1;
@@ -932,7 +952,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 }
 
 static bool fast_seg(const ASeg& g, int Ho, int Wo, int BK) {
-  return g.stride == 1 && !g.up && (g.ks == 1 || g.ks == 3) && g.Hi == Ho && g.Wi == Wo &&
+  return g.stride == 1 && !g.up && (g.ks == 1 || g.ks == 2 || g.ks == 3) && g.Hi == Ho && g.Wi == Wo &&
          g.cin % BK == 0 && (g.c1 == 0 || g.c0 % BK == 0) && g.scale == nullptr;
 }
 
@@ -1026,6 +1046,14 @@ hipError_t launch_gemm(DType dt, const GemmArgs& args, hipStream_t s) {
     return hipErrorInvalidValue;
   if (a.epi.rowscale && dt != BF16) return hipErrorInvalidValue;
   if ((long)a.N * a.ldb * (dt == BF16 ? 2 : 4) >= (1L << 31)) return hipErrorInvalidValue;
+  // upsample phases (ks 2): bf16, the direct-to-LDS tiles (N % 160) with
+  // the uniform-tap loader only
+  const bool phased = a.seg[0].ks == 2 || (a.seg[1].K && a.seg[1].ks == 2);
+  if (phased && (dt != BF16 || a.N % 160 || loader_mode(a, DKS) != 1 || a.ksplit > 1 || a.seg[1].K))
+    return hipErrorInvalidValue;
+  if (a.epi.phase && (a.epi.phase > 4 || a.epi.ph_h < 1 || a.epi.ph_w < 1 || a.M % (a.epi.ph_h * a.epi.ph_w) ||
+                      a.epi.resid || a.epi.vt_out || a.epi.tbias || a.epi.geglu))
+    return hipErrorInvalidValue;
   if (dt == BF16) {
     auto nblk = [&](int bm, int bn) { return (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn); };
     const long want = 2 * 256;

@@ -22,12 +22,14 @@ struct ASeg {
   const float* scale;  // [imgs, cin] or null
   const float* shift;  // [imgs, cin]
   int c0, c1, cin;     // cin = c0 + c1; c0, c1 multiples of 8
-  int ks;              // 1 or 3
+  int ks;              // 1 or 3; 2: one phase of a nearest-2x upsample + 3x3 conv (below)
   int stride;          // 1 or 2
   int up;              // 1: nearest-2x upsample before the conv
   int Hi, Wi, Ho, Wo;  // input (before upsampling) and output sizes
   int K;               // ks * ks * cin
   int silu;
+  int py, px;          // ks == 2: output phase (2 y + py, 2 x + px); tap (ty, tx) reads the
+                       //   input at (y + py - 1 + ty, x + px - 1 + tx), zero outside
 };
 
 // Epilogue: out[m, n] = acc + bias[n] + tbias[row_req... ] + resid[m, n].
@@ -48,6 +50,9 @@ struct Epi {
   long vt_img;
   int qcols;              // columns n < qcols are multiplied by qscale before rounding
   float qscale;           //   (attention queries stored in base-2 logit units)
+  int phase, ph_h, ph_w;  // phase = 1 + 2 py + px: GEMM row m = (image i, y, x) of an ph_h x ph_w
+                          //   grid is output row i (4 ph_h ph_w) + (2 y + py) (2 ph_w) + 2 x + px;
+                          //   0: row m is output row m
   const float* rowscale;  // bf16 only: acc -> rowscale[m] * acc before the bias, or null (the
                           //   LayerNorm rstd of input row m when the LN is folded into the weights)
 };

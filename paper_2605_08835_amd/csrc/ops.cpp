@@ -88,6 +88,32 @@ sd_status synerdiff_op_conv(int32_t dtype, const void* x0, int32_t c0, const voi
   return op_hip(launch_gemm((DType)dtype, a, (hipStream_t)stream), "conv");
 }
 
+sd_status synerdiff_op_upconv(int32_t dtype, const void* x, int32_t n, int32_t H, int32_t W, int32_t cin,
+                              const void* w, int32_t cout, const float* bias, void* out, void* stream) {
+  if (dtype != SD_BF16) return op_fail(SD_ERR_UNSUPPORTED, "upconv is bf16 only");
+  if (!x || !w || !out) return op_fail(SD_ERR_INVALID_ARG, "NULL argument");
+  if (n < 0 || H < 1 || W < 1 || cin < 32 || cin % 32 || cout < 160 || cout % 160)
+    return op_fail(SD_ERR_INVALID_ARG, "bad shape (cin % 32, cout % 160)");
+  if ((long)n * H * W > 0x7FFFFFFFL / 4) return op_fail(SD_ERR_UNSUPPORTED, "too many output pixels");
+  if (n == 0) return SD_OK;
+  for (int ph = 0; ph < 4; ++ph) {
+    GemmArgs a;
+    memset(&a, 0, sizeof(a));
+    ASeg& s = a.seg[0];
+    s.src0 = x; s.c0 = cin; s.cin = cin; s.ks = 2; s.stride = 1;
+    s.Hi = H; s.Wi = W; s.Ho = H; s.Wo = W; s.K = 4 * cin;
+    s.py = ph >> 1; s.px = ph & 1;
+    a.M = n * H * W; a.N = cout; a.K = s.K; a.ldb = s.K;
+    a.B = (const uint8_t*)w + (size_t)ph * cout * s.K * 2;
+    a.ksplit = 1;
+    a.epi.bias = bias; a.epi.out = out; a.epi.ldo = cout; a.epi.hw = 1;
+    a.epi.phase = 1 + ph; a.epi.ph_h = H; a.epi.ph_w = W;
+    const sd_status st = op_hip(launch_gemm(BF16, a, (hipStream_t)stream), "upconv");
+    if (st != SD_OK) return st;
+  }
+  return SD_OK;
+}
+
 sd_status synerdiff_op_attention(int32_t dtype, const void* q, int64_t q_ld, int64_t q_img, const void* k,
                                  int64_t k_ld, int64_t k_img, const void* v, int64_t v_ld, int64_t v_img,
                                  int32_t v_transposed, const int32_t* kv_index, void* o, int64_t o_ld,

@@ -51,7 +51,13 @@ static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // value bias that a folded LayerNorm's shift gives V (names: out bias, out
 // weight, V weight, LN shift): b + W_o (W_v beta).  Attention rows of
 // probabilities sum to one, so a bias on V passes through to the output.
-enum PackKind { P_ACT, P_F32, P_F32_SUM, P_CONV3, P_CONV3_SKIP, P_ACT_GEGLU, P_F32_GEGLU, P_F32_VFOLD };
+// P_UPCONV (bf16): the 3x3 conv that follows a nearest-2x upsample, as four
+// 2x2 convs on the small grid, one per output phase (py, px): tap (ty, tx)
+// of phase (py, px) reads the input at (y + py - 1 + ty, x + px - 1 + tx)
+// and its weight is the sum of the 3x3 taps (ky, kx) that land there,
+// floor((py + ky - 1) / 2) = py - 1 + ty (likewise for x).  Layout
+// [phase][cout][tap][cin].
+enum PackKind { P_ACT, P_F32, P_F32_SUM, P_CONV3, P_CONV3_SKIP, P_ACT_GEGLU, P_F32_GEGLU, P_F32_VFOLD, P_UPCONV };
 struct PackJob {
   PackKind kind;
   size_t dst;
@@ -72,6 +78,7 @@ struct PackJob {
 struct ConvW {
   size_t w = 0, b = 0;
   int cin = 0, cout = 0, K = 0;
+  size_t wp = 0;  // upsampling convs: the four-phase weights (P_UPCONV), or 0
 };
 struct ResW {
   int cin = 0, cout = 0;
@@ -192,6 +199,17 @@ static ConvW conv3(sd_unet* h, const std::string& p, int cin, int cout, int cin_
   h->jobs.push_back(PackJob{P_CONV3, c.w, {p + ".w"}, cin_pad});
   c.b = job_f32(h, {p + ".b"}, cout);
   return c;
+}
+
+// Upsampling conv: the plain 3x3 weights, plus the four-phase form
+// (P_UPCONV) where the GEMM takes it (bf16, width a multiple of 160).
+static ConvW upconv(sd_unet* h, const std::string& p, int c) {
+  ConvW w = conv3(h, p, c, c, c);
+  if (h->dt == BF16 && c % 160 == 0) {
+    w.wp = walloc(h, (size_t)16 * c * c * h->esz);
+    h->jobs.push_back(PackJob{P_UPCONV, w.wp, {p + ".w"}, c});
+  }
+  return w;
 }
 
 static ResW resblock(sd_unet* h, const std::string& p, int cin, int cout, int& tb_off,
@@ -327,7 +345,7 @@ static void build_layout(sd_unet* h) {
     }
     if (l != 0) {
       h->up[l].has_conv = true;
-      h->up[l].conv = conv3(h, p + ".up", cur, cur, cur);
+      h->up[l].conv = upconv(h, p + ".up", cur);
     }
   }
   h->outg = job_f32(h, {"out.norm.g"}, c.ch[0]);
@@ -473,6 +491,7 @@ struct Step {
     a.Wo = up ? 2 * Wi : (stride == 2 ? (Wi - 1) / 2 + 1 : Wi);
     a.K = ks * ks * a.cin;
     a.silu = silu;
+    a.py = a.px = 0;
     return a;
   }
   static ASeg lin(const void* x, int K, long M) { return seg(x, K, nullptr, 0, 1, 1, 0, 1, (int)M, nullptr, nullptr, 0); }
@@ -786,8 +805,24 @@ struct Step {
       if (lv.has_conv) {
         const int nrole = cur_role == R_HA ? R_HB : R_HA;
         void* o = hbuf(nrole, curc, 2 * H, 2 * Wd);
-        gemm(seg(cur, curc, nullptr, 0, 3, 1, 1, H, Wd, nullptr, nullptr, 0), nullptr, W(lv.conv.w), curc,
-             epi(o, curc, Wf(lv.conv.b)), "upsample");
+        if (lv.conv.wp && H * Wd > 64) {
+          // four 2x2 convs on the small grid, one per output phase (4/9 of
+          // the 3x3's products; on 8x8 inputs the phases' grids are too
+          // thin and the 3x3 form measured faster)
+          for (int ph = 0; ph < 4; ++ph) {
+            ASeg sg = seg(cur, curc, nullptr, 0, 2, 1, 0, H, Wd, nullptr, nullptr, 0);
+            sg.py = ph >> 1;
+            sg.px = ph & 1;
+            Epi e = epi(o, curc, Wf(lv.conv.b));
+            e.phase = 1 + ph;
+            e.ph_h = H;
+            e.ph_w = Wd;
+            gemm(sg, nullptr, W(lv.conv.wp) + (size_t)ph * curc * 4 * curc * h->esz, curc, e, "upsample");
+          }
+        } else {
+          gemm(seg(cur, curc, nullptr, 0, 3, 1, 1, H, Wd, nullptr, nullptr, 0), nullptr, W(lv.conv.w), curc,
+               epi(o, curc, Wf(lv.conv.b)), "upsample");
+        }
         cur = o;
         cur_role = nrole;
         H *= 2;
@@ -1084,6 +1119,28 @@ sd_status synerdiff_load_weights(sd_unet* h, const float* hp, size_t n_floats, v
         for (size_t i = 0; i < src[0]->numel; ++i) {
           const float v = hp[src[0]->offset + i] + hp[src[1]->offset + i];
           memcpy(&host[j.dst + i * 4], &v, 4);
+        }
+        break;
+      }
+      case P_UPCONV: {
+        const Param* w = src[0];
+        const int cout = (int)w->shape[0], cin = (int)w->shape[1];
+        const size_t K = 4 * (size_t)cin;
+        auto src_off = [](int p, int k) { return (p + k + 1) / 2 - 1; };  // floor((p + k - 1) / 2)
+        for (int ph = 0; ph < 4; ++ph) {
+          const int py = ph >> 1, px = ph & 1;
+          for (int o = 0; o < cout; ++o)
+            for (int t = 0; t < 4; ++t) {
+              const int dy = py - 1 + (t >> 1), dx = px - 1 + (t & 1);
+              for (int c = 0; c < cin; ++c) {
+                double v = 0.0;
+                for (int ky = 0; ky < 3; ++ky)
+                  for (int kx = 0; kx < 3; ++kx)
+                    if (src_off(py, ky) == dy && src_off(px, kx) == dx)
+                      v += hp[w->offset + ((size_t)o * cin + c) * 9 + ky * 3 + kx];
+                put_act(j.dst, ((size_t)ph * cout + o) * K + (size_t)t * cin + c, (float)v);
+              }
+            }
         }
         break;
       }

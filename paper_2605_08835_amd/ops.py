@@ -60,6 +60,16 @@ def layernorm(x, gamma, beta, eps=1e-5):
     return y
 
 
+def upconv(x, w_phases, cout, bias=None):
+    """Nearest-2x upsample + 3x3 conv of bf16 x [n, H, W, cin] as four phase
+    convolutions; w_phases bf16 [4, cout, 4 * cin]."""
+    n, H, W, cin = x.shape
+    out = torch.empty(n, 2 * H, 2 * W, cout, device=x.device, dtype=x.dtype)
+    _check(lib().synerdiff_op_upconv(_dt(x), _ptr(x), n, H, W, cin, _ptr(w_phases), cout, _ptr(bias), _ptr(out),
+                                     _s()))
+    return out
+
+
 def linear_rows(x, w, bias=None, add=None, silu_in=0, silu_out=0):
     """x fp32 [M, K], w [N, K] (fp32 or bf16) -> fp32 [M, N]."""
     M, K = x.shape

@@ -109,6 +109,54 @@ def test_conv(ops, dt, case, with_resid):
         assert err <= TOL[dt], (i, err)
 
 
+def _phase_weights(w):
+    """[cout, cin, 3, 3] -> [4, cout, 4 cin]: the 2x2 kernel of each output
+    phase (py, px) of a nearest-2x upsample followed by the 3x3 conv (the
+    taps that land on the same input pixel, summed)."""
+    cout, cin = w.shape[:2]
+    out = np.zeros((4, cout, 4, cin), np.float64)
+    for py in range(2):
+        for px in range(2):
+            for ky in range(3):
+                for kx in range(3):
+                    # upsampled row 2y + py + ky - 1 is input row y + (py + ky - 1) // 2
+                    ty, tx = (py + ky - 1) // 2 - (py - 1), (px + kx - 1) // 2 - (px - 1)
+                    out[2 * py + px, :, 2 * ty + tx, :] += w[:, :, ky, kx]
+    return out.reshape(4, cout, 4 * cin)
+
+
+# n, H, W, cin, cout: ragged grids and the SD-1.5 / SDXL upsampling widths
+UPCONV_CASES = [(2, 5, 7, 64, 160), (3, 8, 9, 32, 320), (2, 16, 16, 160, 320), (1, 4, 4, 640, 640),
+                (4, 8, 8, 1280, 1280), (1, 1, 3, 32, 160), (70, 4, 4, 64, 160)]
+
+
+@pytest.mark.parametrize("case", UPCONV_CASES)
+def test_upconv_phases(ops, case):
+    """The four-phase form of upsample + 3x3 conv against the oracle's
+    nearest upsampling and direct convolution (fp64)."""
+    n, H, W, cin, cout = case
+    log(f"upconv {case}")
+    rng = np.random.default_rng(n * 1000 + H * 10 + cin + cout)
+    x = _vals(rng, (n, H, W, cin), "bf16")
+    w = _vals(rng, (cout, cin, 3, 3), "bf16", 1.0 / math.sqrt(9 * cin))
+    b = rng.standard_normal(cout).astype(np.float32)
+    wp = bf16_round(_phase_weights(w.astype(np.float64)).astype(np.float32))
+    got = ops.upconv(_dev(x, "bf16"), _dev(wp, "bf16"), cout, bias=_dev(b))
+    torch.cuda.synchronize()
+    got = got.float().cpu().numpy()
+    for i in range(n):
+        ref = O.conv2d(O.upsample_nearest2x(x[i].astype(np.float64)), w, b, 1)
+        err = rel_l2(got[i], ref)
+        assert err <= TOL["bf16"], (i, err)
+
+
+def test_upconv_rejects_unsupported_widths(ops):
+    x = torch.zeros(1, 4, 4, 32, device="cuda", dtype=torch.bfloat16)
+    w = torch.zeros(4, 36, 4 * 32, device="cuda", dtype=torch.bfloat16)
+    with pytest.raises(RuntimeError):
+        ops.upconv(x, w, 36)
+
+
 @pytest.mark.parametrize("qmode", ["plain", "log2"])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("heads,d,nq,nk,scale,cross", [
