@@ -132,6 +132,9 @@ hipError_t launch_time_inputs(const float* row_t, int rows, int temb_in, float* 
 hipError_t launch_linear_smallm(DType wdt, const float* in, int M, int K, const void* W,
                                 const float* bias, const float* add, float* out, int N,
                                 int silu_in, int silu_out, hipStream_t s);
+// Rows dst0 .. dst0 + n - 1 of a row-major tensor (row_bytes each, a
+// multiple of 16) become copies of rows src_rows[0 .. n - 1].
+hipError_t launch_copy_rows(void* base, long row_bytes, int dst0, int n, const int* src_rows, hipStream_t s);
 hipError_t launch_cfg_ddim(const float* eps_rows, const float* lat_in, float* lat_out,
                            float* eps_out, int n_req, int lc, int hw, const int* req_row_u,
                            const float* req_coef, hipStream_t s);

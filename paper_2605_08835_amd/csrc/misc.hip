@@ -33,6 +33,22 @@ hipError_t launch_pack_latents(DType dt, const float* lat, void* x0, int rows, i
   return hipGetLastError();
 }
 
+__global__ void copy_rows_kernel(uint4* base, long row_vecs, int dst0, const int* src_rows) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= row_vecs) return;
+  const int r = blockIdx.y;
+  base[(long)(dst0 + r) * row_vecs + i] = base[(long)src_rows[r] * row_vecs + i];
+}
+
+hipError_t launch_copy_rows(void* base, long row_bytes, int dst0, int n, const int* src_rows, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (row_bytes % 16) return hipErrorInvalidValue;
+  const long vecs = row_bytes / 16;
+  copy_rows_kernel<<<dim3((unsigned)((vecs + 255) / 256), (unsigned)n), 256, 0, s>>>((uint4*)base, vecs, dst0,
+                                                                                      src_rows);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------ time-embedding inputs
 // Sinusoid [cos(t f_i) | sin(t f_i)], f_i = 10000^(-i/half), evaluated in
 // fp64 so the argument t f_i (up to ~1e3 rad) keeps full fp32 accuracy;

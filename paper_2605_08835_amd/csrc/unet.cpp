@@ -9,6 +9,7 @@
 #include <cmath>
 
 #include <algorithm>
+#include <functional>
 #include <map>
 #include <string>
 #include <vector>
@@ -424,6 +425,21 @@ struct Step {
   bool dry;
   hipStream_t s;
   int n_req, rows;
+  // CFG pairs: until the first cross-attention a request's two rows see the
+  // same latent, timestep and time embedding, so that prefix runs on the
+  // conditional rows only (rows = n_req) and `expand` then copies them into
+  // the unconditional rows (rows = full_rows).  Not with an added
+  // embedding (SDXL's pooled text): there the two rows' time embeddings
+  // differ from the start.  Buffers are sized for full_rows throughout.
+  int full_rows = 0;
+  std::function<void()> expand;
+  const int* d_row_req = nullptr;  // device row plan: row_req[u] is the request of row u
+  // Rows n_req .. full_rows - 1 of tensor t (row_bytes each) <- their requests' rows.
+  void copy_rows(void* t, size_t row_bytes) {
+    if (dry || err || rows >= full_rows) return;
+    ok(launch_copy_rows(t, (long)row_bytes, n_req, full_rows - n_req, d_row_req + n_req, s), "cfg rows", K_COPY, 0,
+       2.0 * (full_rows - n_req) * row_bytes);
+  }
   hipError_t err = hipSuccess;
   const char* where = "";
 
@@ -560,16 +576,17 @@ struct Step {
   // Transformer2D on h (H x W x C), in place.
   void transformer(const TxW& t, void* hbuf, int H, int W_, const void* ctx, const int* row_ctx) {
     const int hw = H * W_, C = t.C;
-    const long T = (long)rows * hw;
+    long T = (long)rows * hw;
+    const long Tmax = (long)std::max(rows, full_rows) * hw;  // buffer sizes
     const int L = h->cfg.ctx_len, D = h->cfg.ctx_dim;
     void* nh = gn_norm(hbuf, C, nullptr, 0, hw, 1e-6f, t.ng, t.nb, 0);
-    void* z = buf(R_TZ, (size_t)T * C * h->esz);
-    void* x = buf(R_TX, (size_t)T * C * h->esz);
-    void* q = buf(R_TQ, (size_t)T * 4 * C * h->esz);
-    void* f = h->dt == BF16 ? nullptr : buf(R_TF, (size_t)T * 8 * C * h->esz);
+    void* z = buf(R_TZ, (size_t)Tmax * C * h->esz);
+    void* x = buf(R_TX, (size_t)Tmax * C * h->esz);
+    void* q = buf(R_TQ, (size_t)Tmax * 4 * C * h->esz);
+    void* f = h->dt == BF16 ? nullptr : buf(R_TF, (size_t)Tmax * 8 * C * h->esz);
     void* ckv = buf(R_CKV, (size_t)(n_req + 1) * L * 2 * C * h->esz);
     const int Lp = (L + 7) / 8 * 8;
-    void* vbuf = h->dt == BF16 ? buf(R_TV, (size_t)T * C * h->esz) : nullptr;
+    void* vbuf = h->dt == BF16 ? buf(R_TV, (size_t)Tmax * C * h->esz) : nullptr;
     void* cvt = h->dt == BF16 ? buf(R_CVT, (size_t)(n_req + 1) * C * Lp * h->esz) : nullptr;
     gemm(lin(nh, C, T), nullptr, W(t.piw), C, epi(z, C, Wf(t.pib)), "proj_in", T);
     // bf16: the three LayerNorms are folded into the projections they feed
@@ -578,7 +595,7 @@ struct Step {
     // computed here and the projections read z itself.  fp32: plain
     // LayerNorm into x.
     const bool fold = h->dt == BF16;
-    float* lns = fold ? (float*)buf(R_LNS, (size_t)T * 4) : nullptr;
+    float* lns = fold ? (float*)buf(R_LNS, (size_t)Tmax * 4) : nullptr;
     auto layernorm = [&](size_t g, size_t bb, const char* name) -> const void* {
       if (fold) {
         if (!dry && !err) ok(launch_layernorm_rstd(h->dt, z, lns, T, C, 1e-5f, s), name, K_LN, 4.0 * T * C, (double)T * C * h->esz + 4.0 * T);
@@ -634,6 +651,12 @@ struct Step {
            4.0 * T * C * h->esz);
       }
       gemm(lin(x, C, T), nullptr, W(b.o1w), C, epi(z, C, Wf(b.o1b), z, C), "attn1.out", T);
+      if (expand) {  // the rows diverge at the cross-attention: fill in the unconditional ones
+        copy_rows(z, (size_t)hw * C * h->esz);
+        expand();
+        expand = nullptr;
+        T = (long)rows * hw;
+      }
       {
         const void* xin2 = layernorm(b.ln2g, b.ln2b, "ln2");
         Epi e2 = epi(q, C, nullptr);
@@ -743,19 +766,33 @@ struct Step {
       ok(launch_linear_smallm(h->dt, tau, rows, td, W(h->tbw), Wf(h->tbb), nullptr, tb, h->tb_total, 1, 0, s), "temb",
          K_TIME, 2.0 * rows * td * h->tb_total, (double)td * h->tb_total * h->esz + 4.0 * rows * h->tb_total);
     }
+    // conditional rows only until the first cross-attention (see `expand`)
+    full_rows = rows;
+    d_row_req = row_req;
+    if (rows > n_req && c.add_in == 0) rows = n_req;
     // pack + conv_in
-    void* x0 = buf(R_X0, (size_t)rows * H * Wd * h->cpad * h->esz);
+    void* x0 = buf(R_X0, (size_t)full_rows * H * Wd * h->cpad * h->esz);
     if (!dry && !err)
       ok(launch_pack_latents(h->dt, lat_in, x0, rows, c.latent_c, H * Wd, h->cpad, row_req, s), "pack", K_PACK, 0,
          4.0 * n_req * c.latent_c * H * Wd + (double)rows * H * Wd * h->cpad * h->esz);
     std::vector<void*> skip(h->n_skips);
     std::vector<int> skipc(h->n_skips);
+    std::vector<size_t> skiprow(h->n_skips);
     int k = 0;
     auto skipbuf = [&](int ch, int hh, int ww) {
       skipc[k] = ch;
-      skip[k] = buf(R_SKIP0 + k, (size_t)rows * hh * ww * ch * h->esz);
+      skiprow[k] = (size_t)hh * ww * ch * h->esz;
+      skip[k] = buf(R_SKIP0 + k, (size_t)full_rows * skiprow[k]);
       return skip[k++];
     };
+    // the live tensors at the first cross-attention are the skip stack so
+    // far (the transformer's input is its last entry) and the transformer's z
+    if (rows < full_rows) {
+      expand = [&]() {
+        for (int i = 0; i < k; ++i) copy_rows(skip[i], skiprow[i]);
+        rows = full_rows;
+      };
+    }
     void* cur = skipbuf(c.ch[0], H, Wd);
     gemm(seg(x0, h->cpad, nullptr, 0, 3, 1, 0, H, Wd, nullptr, nullptr, 0), nullptr, W(h->conv_in.w), c.ch[0],
          epi(cur, c.ch[0], Wf(h->conv_in.b)), "conv_in", -1, 9.0 * c.latent_c);
@@ -779,6 +816,10 @@ struct Step {
         H = Ho;
         Wd = Wo;
       }
+    }
+    if (expand) {  // (no cross-attention on the down path)
+      expand();
+      expand = nullptr;
     }
     // hidden ping-pong buffers
     auto hbuf = [&](int role, int ch, int hh, int ww) { return buf(role, (size_t)rows * hh * ww * ch * h->esz); };
