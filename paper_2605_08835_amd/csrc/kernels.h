@@ -128,7 +128,7 @@ hipError_t launch_time_inputs(const float* row_t, int rows, int temb_in, float* 
                               const int* row_req, const int* row_branch, int pooled_dim,
                               const float* time_ids_dev, int n_ids, int id_dim, float* a,
                               hipStream_t s);
-// out[m, n] = act_out(sum_k act_in(in[m, k]) W[n, k] + bias[n] + add[m, n]); M <= 128.
+// out[m, n] = act_out(sum_k act_in(in[m, k]) W[n, k] + bias[n] + add[m, n]) for a few rows; K % 4 == 0.
 hipError_t launch_linear_smallm(DType wdt, const float* in, int M, int K, const void* W,
                                 const float* bias, const float* add, float* out, int N,
                                 int silu_in, int silu_out, hipStream_t s);
