@@ -352,16 +352,17 @@ hipError_t launch_groupnorm_stats(DType dt, const void* src0, int c0, const void
 
 // Pass 3: y = act(x * scale + shift) into a materialised [imgs, hw, cin]
 // tensor (the concat of the two sources when there are two); one 8-channel
-// vector per thread.
+// vector per thread, blockIdx.y the image (32-bit index arithmetic).
 template <typename T>
 __global__ void gn_apply_kernel(const T* src0, int c0, const T* src1, int c1, const float* scale,
-                                const float* shift, T* out, long n_vec, int hw, int silu) {
-  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n_vec) return;
+                                const float* shift, T* out, int hw, int silu) {
   const int cin = c0 + c1, CV = cin / 8;
-  const long pix = i / CV;
-  const int c = (int)(i - pix * CV) * 8;
-  const int img = (int)(pix / hw);
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= hw * CV) return;
+  const int img = blockIdx.y;
+  const int p = i / CV;
+  const int c = (i - p * CV) * 8;
+  const long pix = (long)img * hw + p;
   float v[8], sc[8], sh[8];
   if (c < c0)
     load8f(src0 + pix * c0 + c, v);
@@ -380,15 +381,16 @@ __global__ void gn_apply_kernel(const T* src0, int c0, const T* src1, int c1, co
 hipError_t launch_groupnorm_apply(DType dt, const void* src0, int c0, const void* src1, int c1, int imgs,
                                   int hw, const float* scale, const float* shift, int silu, void* out,
                                   hipStream_t s) {
-  const long n = (long)imgs * hw * ((c0 + c1) / 8);
-  if (n == 0) return hipSuccess;
-  const unsigned blocks = (unsigned)((n + 255) / 256);
+  const long per_img = (long)hw * ((c0 + c1) / 8);
+  if (imgs == 0 || per_img == 0) return hipSuccess;
+  if (per_img >= (1L << 31) || imgs > 65535) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)((per_img + 255) / 256), (unsigned)imgs);
   if (dt == BF16)
-    gn_apply_kernel<bf16><<<blocks, 256, 0, s>>>((const bf16*)src0, c0, (const bf16*)src1, c1, scale, shift,
-                                                 (bf16*)out, n, hw, silu);
+    gn_apply_kernel<bf16><<<grid, 256, 0, s>>>((const bf16*)src0, c0, (const bf16*)src1, c1, scale, shift,
+                                               (bf16*)out, hw, silu);
   else
-    gn_apply_kernel<float><<<blocks, 256, 0, s>>>((const float*)src0, c0, (const float*)src1, c1, scale,
-                                                  shift, (float*)out, n, hw, silu);
+    gn_apply_kernel<float><<<grid, 256, 0, s>>>((const float*)src0, c0, (const float*)src1, c1, scale, shift,
+                                                (float*)out, hw, silu);
   return hipGetLastError();
 }
 
