@@ -1058,13 +1058,16 @@ hipError_t launch_gemm(DType dt, const GemmArgs& args, hipStream_t s) {
     auto nblk = [&](int bm, int bn) { return (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn); };
     const long want = 2 * 256;
     if (a.N % 160 == 0) {
-      // 256x160 tiles through the two-stage direct-to-LDS pipeline whenever
-      // the loader is uniform: taller tiles cut the weight re-reads that
-      // dominate small-M layers, and two stages leave LDS for two blocks.
-      // Otherwise register-staged 64-deep tiles, one block per CU.
+      // 256x160 tiles through the direct-to-LDS pipeline whenever the loader
+      // is uniform: taller tiles cut the weight re-reads that dominate
+      // small-M layers.  Three K stages (two for the split-K layers) still
+      // leave LDS for two blocks per CU.  Otherwise register-staged 64-deep
+      // tiles, one block per CU.
       const bool big = nblk(256, 160) * a.ksplit >= want;
       if (a.ksplit == 1 && nblk(256, 160) < 256 && launch_dma<64, 160, 2, 1, 2, 4>(a, s)) {
         // short M (the context K/V projections): 64-row tiles, four blocks per CU
+      } else if (a.ksplit == 1 && launch_dma<256, 160, 4, 1, 3, 2>(a, s)) {
+        // three K stages (2 x 79.9 KB of LDS: still two blocks per CU)
       } else if (launch_dma<256, 160, 4, 1, 2, 2>(a, s)) {
       } else if (big) {
         launch_bf16<256, 160, 64, 4, 1>(a, s);
