@@ -92,6 +92,16 @@ sd_status synerdiff_op_groupnorm_stats(int32_t dtype, const void* d_x0, int32_t 
 sd_status synerdiff_op_layernorm(int32_t dtype, const void* d_x, void* d_y, int64_t tokens, int32_t C,
                                  const float* d_gamma, const float* d_beta, float eps, void* hip_stream);
 
+/* The LayerNorm scale alone, rstd[t] = 1 / sqrt(var_t + eps) with the
+ * biased variance of token t of x [tokens, C] (C a multiple of 8, <= 2048):
+ * the per-token factor of the SD transformer blocks' LayerNorms when their
+ * mean, gain and shift are folded into the projection weights (the
+ * latent-diffusion UNet the paper serves, Sec. IV-A).  rstd is fp32
+ * [tokens], device memory owned by the caller; nothing else is written.
+ * tokens = 0 does nothing. */
+sd_status synerdiff_op_layernorm_rstd(int32_t dtype, const void* d_x, float* d_rstd, int64_t tokens, int32_t C,
+                                      float eps, void* hip_stream);
+
 /* Linear layer over a few fp32 rows, the per-request timestep-embedding
  * MLP and time projections of the latent-diffusion UNet the paper serves
  * (Sec. IV-A):

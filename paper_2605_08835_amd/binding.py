@@ -80,6 +80,8 @@ _SIG = {
                                      [ctypes.c_float, _P, _P, _P, _P, _P, _P]),
     "synerdiff_op_layernorm": (ctypes.c_int, [ctypes.c_int32, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P,
                                               ctypes.c_float, _P]),
+    "synerdiff_op_layernorm_rstd": (ctypes.c_int, [ctypes.c_int32, _P, _P, ctypes.c_int64, ctypes.c_int32,
+                                                    ctypes.c_float, _P]),
     "synerdiff_op_geglu": (ctypes.c_int, [ctypes.c_int32, _P, _P, ctypes.c_int64, ctypes.c_int32, _P]),
     "synerdiff_op_upconv": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                            ctypes.c_int32, _P, ctypes.c_int32, _P, _P, _P]),

@@ -167,6 +167,16 @@ sd_status synerdiff_op_layernorm(int32_t dtype, const void* x, void* y, int64_t 
   return op_hip(launch_layernorm((DType)dtype, x, y, tokens, C, gamma, beta, eps, (hipStream_t)stream), "layernorm");
 }
 
+sd_status synerdiff_op_layernorm_rstd(int32_t dtype, const void* x, float* rstd, int64_t tokens, int32_t C,
+                                      float eps, void* stream) {
+  if (bad_dtype(dtype)) return op_fail(SD_ERR_INVALID_ARG, "bad dtype");
+  if (tokens < 0 || C < 8 || C % 8 || C > 2048) return op_fail(SD_ERR_INVALID_ARG, "bad shape");
+  if (tokens == 0) return SD_OK;
+  if (!x || !rstd) return op_fail(SD_ERR_INVALID_ARG, "NULL argument");
+  return op_hip(launch_layernorm_rstd((DType)dtype, x, rstd, tokens, C, eps, (hipStream_t)stream),
+                "layernorm_rstd");
+}
+
 sd_status synerdiff_op_linear_rows(int32_t dtype, const float* in, int32_t M, int32_t K, const void* w,
                                    const float* bias, const float* add, float* out, int32_t N, int32_t silu_in,
                                    int32_t silu_out, void* stream) {

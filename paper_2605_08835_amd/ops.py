@@ -60,6 +60,14 @@ def layernorm(x, gamma, beta, eps=1e-5):
     return y
 
 
+def layernorm_rstd(x, eps=1e-5):
+    """fp32 [tokens] = 1 / sqrt(var + eps) of each row of x [tokens, C]."""
+    C = x.shape[-1]
+    rstd = torch.empty(x.numel() // C, device=x.device)
+    _check(lib().synerdiff_op_layernorm_rstd(_dt(x), _ptr(x), _ptr(rstd), x.numel() // C, C, float(eps), _s()))
+    return rstd
+
+
 def upconv(x, w_phases, cout, bias=None):
     """Nearest-2x upsample + 3x3 conv of bf16 x [n, H, W, cin] as four phase
     convolutions; w_phases bf16 [4, cout, 4 * cin]."""

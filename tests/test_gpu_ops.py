@@ -250,6 +250,29 @@ def test_layernorm(ops, dt, T, C):
     assert err <= (2e-6 if dt == "f32" else 6e-3), err
 
 
+# every tokens-per-wave variant (C <= 512: 4 tokens per wave; wider: 2, with
+# 2-4 vectors per lane) and token counts that end inside a wave's group
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("T,C", [(1, 8), (19, 40), (1003, 320), (6, 512), (9, 640), (131, 1280), (7, 2048),
+                                 (0, 320)])
+def test_layernorm_rstd(ops, dt, T, C):
+    log(f"layernorm_rstd {dt} {(T, C)}")
+    rng = np.random.default_rng(7 * T + C)
+    x = _vals(rng, (T, C), dt, 3.0) + _vals(rng, (T, 1), dt, 2.0)
+    x = bf16_round(x) if dt == "bf16" else x
+    r = ops.layernorm_rstd(_dev(x, dt))
+    torch.cuda.synchronize()
+    r = r.cpu().numpy().astype(np.float64)
+    assert r.shape == (T,)
+    if T == 0:
+        return
+    # (x - mean) * rstd is the oracle's LayerNorm with unit gain and no shift
+    xd = x.astype(np.float64)
+    got = (xd - xd.mean(axis=1, keepdims=True)) * r[:, None]
+    err = rel_l2(got, O.layer_norm(xd, np.ones(C), np.zeros(C)))
+    assert err <= 2e-6, err
+
+
 def _silu(x):
     return x / (1.0 + np.exp(-x))
 
