@@ -97,6 +97,12 @@ hipError_t launch_groupnorm_stats(DType dt, const void* src0, int c0, const void
                                   hipStream_t s);
 size_t groupnorm_partial_floats(int imgs, int hw, int cin);
 // out = act(x * scale + shift) over the concat [src0 | src1] (act = SiLU or identity).
+// Statistics and apply in one launch for small images (bf16; see
+// groupnorm_fused_ok for the shapes it takes).
+bool groupnorm_fused_ok(DType dt, int c0, int c1, int hw, int groups);
+hipError_t launch_groupnorm_fused(DType dt, const void* src0, int c0, const void* src1, int c1, int imgs, int hw,
+                                  int groups, float eps, const float* gamma, const float* beta, int silu, void* out,
+                                  hipStream_t s);
 hipError_t launch_groupnorm_apply(DType dt, const void* src0, int c0, const void* src1, int c1, int imgs,
                                   int hw, const float* scale, const float* shift, int silu, void* out,
                                   hipStream_t s);

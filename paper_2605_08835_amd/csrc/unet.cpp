@@ -478,6 +478,14 @@ struct Step {
 
   // GroupNorm (+ SiLU) of [src0 | src1] materialised as one [rows, hw, cin] tensor.
   void* gn_norm(const void* s0, int c0, const void* s1, int c1, int hw, float eps, size_t g, size_t b, int silu) {
+    if (hw <= 256 && groupnorm_fused_ok(h->dt, c0, c1, hw, h->cfg.gn_groups)) {
+      const int cin = c0 + c1;
+      void* out = buf(R_GNA, (size_t)rows * hw * cin * h->esz);
+      if (dry || err) return out;
+      ok(launch_groupnorm_fused(h->dt, s0, c0, s1, c1, rows, hw, h->cfg.gn_groups, eps, Wf(g), Wf(b), silu, out, s),
+         "groupnorm fused", K_GN, (silu ? 9.0 : 5.0) * rows * hw * cin, 2.0 * rows * hw * cin * h->esz);
+      return out;
+    }
     float *sc, *sh;
     gn(s0, c0, s1, c1, hw, eps, g, b, &sc, &sh);
     const int cin = c0 + c1;
