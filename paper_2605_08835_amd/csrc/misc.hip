@@ -399,28 +399,35 @@ hipError_t launch_groupnorm_apply(DType dt, const void* src0, int c0, const void
 // Small images (at most 5120 four-channel vectors per (image, group), the
 // 16x16 and 8x8 levels of the SD UNets): statistics and apply in one kernel,
 // one block per (group, image).  The block keeps its group's values in
-// registers (E 4-channel vectors per thread, 8-byte loads; a group's
-// channels are consecutive, a vector never straddles the two sources),
-// adds the fp32 per-thread sums in fp64 across the block, and writes
-// act(x * scale + shift) with the same per-channel scale and shift as the
-// three-pass form.  One launch instead of three, and one read of the input.
-template <int E>
+// registers (E vectors of W = 8 channels per thread, 16-byte loads, where
+// the group width and the sources' widths are multiples of 8, else W = 4
+// and 8-byte loads; a group's channels are consecutive, a vector never
+// straddles the two sources), adds the fp32 per-thread sums in fp64 across
+// the block, and writes act(x * scale + shift) with the same per-channel
+// scale and shift as the three-pass form.  One launch instead of three, and
+// one read of the input.
+template <int W> struct bvec;
+template <> struct bvec<4> { typedef bf16x4 type; };
+template <> struct bvec<8> { typedef bf16x8 type; };
+
+template <int E, int W>
 __global__ __launch_bounds__(256) void gn_fused_kernel(const bf16* src0, int c0, const bf16* src1, int c1,
                                                        int hw, int groups, float eps, const float* gamma,
                                                        const float* beta, int silu, bf16* out) {
+  typedef typename bvec<W>::type vec;
   const int g = blockIdx.x, img = blockIdx.y, tid = threadIdx.x;
-  const int cin = c0 + c1, cpg = cin / groups, V = cpg / 4, n = hw * V, cg = g * cpg;
-  float v[E][4];
+  const int cin = c0 + c1, cpg = cin / groups, V = cpg / W, n = hw * V, cg = g * cpg;
+  float v[E][W];
   float s = 0.f, q = 0.f;
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int i = tid + 256 * e;
     if (i < n) {
-      const int p = i / V, c = cg + (i - p * V) * 4;
+      const int p = i / V, c = cg + (i - p * V) * W;
       const bf16* src = c < c0 ? src0 + ((long)img * hw + p) * c0 + c : src1 + ((long)img * hw + p) * c1 + (c - c0);
-      const bf16x4 a = *reinterpret_cast<const bf16x4*>(src);
+      const vec a = *reinterpret_cast<const vec*>(src);
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
+      for (int k = 0; k < W; ++k) {
         v[e][k] = (float)a[k];
         s += v[e][k];
         q = fmaf(v[e][k], v[e][k], q);
@@ -445,16 +452,16 @@ __global__ __launch_bounds__(256) void gn_fused_kernel(const bf16* src0, int c0,
   for (int e = 0; e < E; ++e) {
     const int i = tid + 256 * e;
     if (i < n) {
-      const int p = i / V, c = cg + (i - p * V) * 4;
-      bf16x4 o;
+      const int p = i / V, c = cg + (i - p * V) * W;
+      vec o;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
+      for (int k = 0; k < W; ++k) {
         const float sc = gamma[c + k] * rstd;
         float y = v[e][k] * sc + (beta[c + k] - (float)mean * sc);
         if (silu) y = silu_f(y);
         o[k] = (bf16)y;
       }
-      *reinterpret_cast<bf16x4*>(out + ((long)img * hw + p) * cin + c) = o;
+      *reinterpret_cast<vec*>(out + ((long)img * hw + p) * cin + c) = o;
     }
   }
 }
@@ -471,15 +478,27 @@ hipError_t launch_groupnorm_fused(DType dt, const void* src0, int c0, const void
                                   hipStream_t s) {
   if (!groupnorm_fused_ok(dt, c0, c1, hw, groups) || imgs > 65535) return hipErrorInvalidValue;
   if (imgs == 0 || hw == 0) return hipSuccess;
-  const long n = (long)hw * ((c0 + c1) / groups / 4);
+  const int cpg = (c0 + c1) / groups;
   const dim3 grid(groups, imgs);
   const bf16 *a = (const bf16*)src0, *b = (const bf16*)src1;
-  if (n <= 256 * 4)
-    gn_fused_kernel<4><<<grid, 256, 0, s>>>(a, c0, b, c1, hw, groups, eps, gamma, beta, silu, (bf16*)out);
-  else if (n <= 256 * 8)
-    gn_fused_kernel<8><<<grid, 256, 0, s>>>(a, c0, b, c1, hw, groups, eps, gamma, beta, silu, (bf16*)out);
-  else
-    gn_fused_kernel<20><<<grid, 256, 0, s>>>(a, c0, b, c1, hw, groups, eps, gamma, beta, silu, (bf16*)out);
+  bf16* o = (bf16*)out;
+  if (cpg % 8 == 0 && c0 % 8 == 0 && c1 % 8 == 0) {
+    const long n = (long)hw * (cpg / 8);  // <= 2560
+    if (n <= 256 * 4)
+      gn_fused_kernel<4, 8><<<grid, 256, 0, s>>>(a, c0, b, c1, hw, groups, eps, gamma, beta, silu, o);
+    else if (n <= 256 * 8)
+      gn_fused_kernel<8, 8><<<grid, 256, 0, s>>>(a, c0, b, c1, hw, groups, eps, gamma, beta, silu, o);
+    else
+      gn_fused_kernel<10, 8><<<grid, 256, 0, s>>>(a, c0, b, c1, hw, groups, eps, gamma, beta, silu, o);
+  } else {
+    const long n = (long)hw * (cpg / 4);  // <= 5120
+    if (n <= 256 * 4)
+      gn_fused_kernel<4, 4><<<grid, 256, 0, s>>>(a, c0, b, c1, hw, groups, eps, gamma, beta, silu, o);
+    else if (n <= 256 * 8)
+      gn_fused_kernel<8, 4><<<grid, 256, 0, s>>>(a, c0, b, c1, hw, groups, eps, gamma, beta, silu, o);
+    else
+      gn_fused_kernel<20, 4><<<grid, 256, 0, s>>>(a, c0, b, c1, hw, groups, eps, gamma, beta, silu, o);
+  }
   return hipGetLastError();
 }
 
