@@ -478,6 +478,8 @@ struct Step {
 
   // GroupNorm (+ SiLU) of [src0 | src1] materialised as one [rows, hw, cin] tensor.
   void* gn_norm(const void* s0, int c0, const void* s1, int c1, int hw, float eps, size_t g, size_t b, int silu) {
+    // images of 16x16 and smaller: one fused kernel (on the 640-channel
+    // tensors at 32x32, which it would also take, the three passes are faster)
     if (hw <= 256 && groupnorm_fused_ok(h->dt, c0, c1, hw, h->cfg.gn_groups)) {
       const int cin = c0 + c1;
       void* out = buf(R_GNA, (size_t)rows * hw * cin * h->esz);
