@@ -54,10 +54,42 @@ def kernel_class(name):
     for key, cls in (("gemm_bf16", "gemm"), ("gemm_f32", "gemm"), ("splitk_reduce", "gemm"),
                      ("attn_", "attention"), ("gn_apply", "groupnorm apply"), ("gn_", "groupnorm"),
                      ("layernorm", "layernorm"), ("geglu", "geglu"), ("linear_smallm", "time_mlp"),
-                     ("time_inputs", "time_mlp"), ("pack_latents", "pack"), ("cfg_ddim", "cfg_ddim")):
+                     ("time_inputs", "time_mlp"), ("pack_latents", "pack"), ("out_cfg_ddim", "out_cfg_ddim"),
+                     ("cfg_ddim", "cfg_ddim")):
         if key in name:
             return cls
     return None
+
+
+def non_gemm_flops_per_row(unet):
+    """Algorithmic FLOPs per UNet row that are not GEMM-class work: the
+    attention cores (Q K^T and P V: 4 N_q N_k C per Transformer block, self-
+    and cross-attention) and the output conv (3x3, C0 -> latent channels),
+    which the fused output kernel computes.  The rest of the per-row total is
+    the convolutions and linears the GEMM kernel runs."""
+    H, W = unet["latent_h"], unet["latent_w"]
+    L = unet["ctx_len"]
+    f = 0.0
+    for l, C in enumerate(unet["ch"]):
+        n = (H >> l) * (W >> l)
+        blocks = (2 * unet["n_res"] + 1) * unet["tx_depth"][l]  # down: n_res, up: n_res + 1
+        f += blocks * 4.0 * n * (n + L) * C
+    n = (H >> (len(unet["ch"]) - 1)) * (W >> (len(unet["ch"]) - 1))
+    f += unet["mid_tx_depth"] * 4.0 * n * (n + L) * unet["ch"][-1]
+    out_conv = 2.0 * H * W * 9 * unet["ch"][0] * unet["latent_c"]
+    return f, out_conv
+
+
+def cpu_description():
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return os.cpu_count(), model
 
 
 def source_digest(path):
@@ -163,9 +195,12 @@ def cpu_baseline(unet, weights, req, budget_s=25.0):
         if time.perf_counter() - t0 >= budget_s:
             break
     el = time.perf_counter() - t0
+    ncpu, model = cpu_description()
     return {"value": rows / el, "unit": "rows·steps/s", "cores": int(cores), "kind": "oracle",
             "sample": f"{len(done)} requests ({rows} UNet rows) of the same {len(req['cfg_on'])}-request batch, "
-                      f"one full float64 step each, {el:.1f} s"}
+                      f"one full float64 step each, {el:.1f} s",
+            "host_cpu_count": ncpu, "host_cpu_model": model,
+            "cores_note": "cores = BLAS threads the oracle's float64 products ran on"}
 
 
 def main():
@@ -275,14 +310,23 @@ def main():
                       "gbps": v["bytes"] / max(v["ms"], 1e-9) / 1e6}
     g = prof.get("gemm", {"launches": 1, "ms": 1.0, "flop": 0.0, "bytes": 0.0})
     g_launches = g["launches"] / args.steps
-    flop_per_launch = g["flop"] / max(g["launches"], 1)
     avg_s = g["ms"] / max(g["launches"], 1) / 1e3
+    # Algorithmic FLOPs of the GEMM class: every conv and linear of the
+    # model at its full size (each upsampling conv as a 3x3 on the upsampled
+    # grid, every row's CFG prefix), i.e. the per-row total less the
+    # attention cores and the output conv, times the rows, per launch.
+    attn_row, out_row = non_gemm_flops_per_row(unet)
+    gemm_row = flop_per_row - attn_row - out_row
+    flop_per_launch = rows * gemm_row / max(g_launches, 1e-9)
     achieved = flop_per_launch / avg_s / 1e12
-    roof = {"kernel": "gemm_bf16_kernel (implicit-GEMM conv / linear, MFMA 32x32x16 bf16)",
+    exec_per_launch = g["flop"] / max(g["launches"], 1)
+    roof = {"kernel": "gemm_bf16_dma_kernel (implicit-GEMM conv / linear, MFMA 32x32x16 bf16)",
             "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
             "frac": round(achieved * 1e12 / PEAK_BF16, 4), "traffic": stored_traffic() if wl == WORKLOAD else None,
-            "flop_per_launch": flop_per_launch, "launches_per_step": g_launches,
-            "avg_launch_us": round(avg_s * 1e6, 2)}
+            "flop_per_launch": flop_per_launch, "gemm_flop_per_row": gemm_row, "launches_per_step": g_launches,
+            "avg_launch_us": round(avg_s * 1e6, 2),
+            "executed_flop_per_launch": exec_per_launch,
+            "executed_frac": round(exec_per_launch / avg_s / PEAK_BF16, 4)}
 
     value = rows * 1e3 / ms
     res = {

@@ -87,6 +87,19 @@ sd_status synerdiff_op_groupnorm_stats(int32_t dtype, const void* d_x0, int32_t 
                                        const float* d_gamma, const float* d_beta, float* d_partial,
                                        float* d_scale, float* d_shift, void* hip_stream);
 
+/* GroupNorm of the concat [x0 | x1] ([n, hw, c0 + c1], `groups` groups of
+ * consecutive channels, biased variance, eps) followed by SiLU when silu =
+ * 1, written to out [n, hw, c0 + c1]: the normalisation in front of every
+ * ResBlock conv of the latent-diffusion UNet the paper serves (Sec. IV-A),
+ * as the step runs it on its small images, statistics and apply in one
+ * kernel (one block per (group, image)).  bf16 only; the channels per group
+ * a multiple of 4, c0 and c1 multiples of 4, and hw * (channels per group)
+ * / 4 <= 5120 (SD_ERR_UNSUPPORTED otherwise).  gamma, beta fp32 [c0 + c1].
+ * n = 0 does nothing. */
+sd_status synerdiff_op_groupnorm_fused(int32_t dtype, const void* d_x0, int32_t c0, const void* d_x1, int32_t c1,
+                                       int32_t n, int32_t hw, int32_t groups, float eps, const float* d_gamma,
+                                       const float* d_beta, int32_t silu, void* d_out, void* hip_stream);
+
 /* LayerNorm over the last axis of x [tokens, C] (biased variance):
  * y = (x - mean) * rstd * gamma + beta.  C a multiple of 8, <= 2048. */
 sd_status synerdiff_op_layernorm(int32_t dtype, const void* d_x, void* d_y, int64_t tokens, int32_t C,
@@ -118,6 +131,29 @@ sd_status synerdiff_op_linear_rows(int32_t dtype, const float* d_in, int32_t M, 
  * [tokens, 2*half], y [tokens, half]; half a multiple of 8. */
 sd_status synerdiff_op_geglu(int32_t dtype, const void* d_x, void* d_y, int64_t tokens, int32_t half,
                              void* hip_stream);
+
+/* The step's last stage as one kernel: the UNet's output convolution, the
+ * classifier-free guidance combine and the DDIM update (CFG as in Ho &
+ * Salimans 2022; Skip-CFG bypasses the unconditional branch, Sec. II-B and
+ * Sec. III-B; DDIM eta = 0, Song et al. 2021).  For request r < n_req and
+ * each pixel p, channel o < 4:
+ *   eps_c = b[o] + sum_{ky, kx, c} x[r, y + ky - 1, x + kx - 1, c] w[o, (3 ky + kx) C + c]
+ *   (zero outside the image); eps_u likewise from row req_row_u[r] when it
+ *   is >= 0; eps = eps_u + w_r (eps_c - eps_u) if so, else eps_c;
+ *   lat_out[r, o, p] = A_r lat_in[r, o, p] + B_r eps;  eps_out (if not NULL) = eps.
+ * x: device bf16 [rows, H, W, C] (rows covering every index used), the
+ * normalised (GroupNorm + SiLU) input of the output conv.  w: device bf16
+ * [4][9 C] (the layout synerdiff_op_conv takes), bias fp32 [4].
+ * d_req_row_u: device int32 [n_req]; d_req_coef: device fp32 [n_req, 3] =
+ * (A_r, B_r, w_r).  lat_in, lat_out, eps_out: device fp32 [n_req, 4, H, W]
+ * (NCHW); lat_out may equal lat_in, eps_out must not overlap either.
+ * dtype must be SD_BF16; C a multiple of 32 and <= 320, W <= 128
+ * (SD_ERR_UNSUPPORTED otherwise).  n_req = 0 does nothing. */
+sd_status synerdiff_op_conv_out_cfg_ddim(int32_t dtype, const void* d_x, int32_t H, int32_t W, int32_t C,
+                                         const void* d_w, const float* d_bias, int32_t n_req,
+                                         const int32_t* d_req_row_u, const float* d_req_coef,
+                                         const float* d_lat_in, float* d_lat_out, float* d_eps_out,
+                                         void* hip_stream);
 
 #ifdef __cplusplus
 }

@@ -78,6 +78,11 @@ _SIG = {
     "synerdiff_op_groupnorm_scratch_floats": (ctypes.c_size_t, [ctypes.c_int32] * 3),
     "synerdiff_op_groupnorm_stats": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, _P] + [ctypes.c_int32] * 4 +
                                      [ctypes.c_float, _P, _P, _P, _P, _P, _P]),
+    "synerdiff_op_conv_out_cfg_ddim": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, ctypes.c_int32,
+                                                      ctypes.c_int32, _P, _P, ctypes.c_int32, _P, _P, _P, _P, _P,
+                                                      _P]),
+    "synerdiff_op_groupnorm_fused": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, _P] + [ctypes.c_int32] * 4 +
+                                     [ctypes.c_float, _P, _P, ctypes.c_int32, _P, _P]),
     "synerdiff_op_layernorm": (ctypes.c_int, [ctypes.c_int32, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P,
                                               ctypes.c_float, _P]),
     "synerdiff_op_layernorm_rstd": (ctypes.c_int, [ctypes.c_int32, _P, _P, ctypes.c_int64, ctypes.c_int32,
@@ -220,18 +225,71 @@ class UNet:
         """Enqueue one step.  latents, ctx_*, pooled_*, out and eps_out are
         device tensors; timesteps, cfg_on, guidance, coef and time_ids are
         host arrays.  Returns out."""
-        n = int(latents.shape[0])
-        ts = np.ascontiguousarray(timesteps, np.int32)
-        cf = np.ascontiguousarray(cfg_on, np.uint8)
-        gd = np.ascontiguousarray(guidance, np.float32)
-        cc = np.ascontiguousarray(coef, np.float32).reshape(-1)
-        ti = None if time_ids is None else np.ascontiguousarray(time_ids, np.float32)
+        n = int(latents.shape[0]) if hasattr(latents, "shape") and len(latents.shape) else -1
+        u = self.unet
+        lat_shape = (n, u["latent_c"], u["latent_h"], u["latent_w"])
+        L, D = u["ctx_len"], u["ctx_dim"]
+        f32 = self.torch.float32
+        self._check_dev("latents", latents, lat_shape, f32)
+        ts = self._host("timesteps", timesteps, np.int32, (n,))
+        cf = self._host("cfg_on", cfg_on, np.uint8, (n,))
+        gd = self._host("guidance", guidance, np.float32, (n,))
+        cc = self._host("coef", coef, np.float32, (n, 2)).reshape(-1)
+        self._check_dev("ctx_cond", ctx_cond, (n, L, D), self.act_dtype)
+        if ctx_uncond is not None:
+            shp = tuple(ctx_uncond.shape) if hasattr(ctx_uncond, "shape") else None
+            self._check_dev("ctx_uncond", ctx_uncond, (1, L, D) if shp and len(shp) == 3 else (L, D),
+                            self.act_dtype)
+        if u["add_in"]:
+            P = u["pooled_dim"]
+            self._check_dev("pooled_cond", pooled_cond, (n, P), f32)
+            if pooled_uncond is not None:
+                shp = tuple(pooled_uncond.shape) if hasattr(pooled_uncond, "shape") else None
+                self._check_dev("pooled_uncond", pooled_uncond, (1, P) if shp and len(shp) == 2 else (P,), f32)
+            ti = self._host("time_ids", time_ids, np.float32, (u["n_time_ids"],))
+        else:
+            if pooled_cond is not None or pooled_uncond is not None or time_ids is not None:
+                raise ValueError("pooled inputs / time_ids given but the UNet has no added embedding")
+            ti = None
         if out is None:
             out = self.torch.empty_like(latents)
+        else:
+            self._check_dev("out", out, lat_shape, f32)
+        if eps_out is not None:
+            self._check_dev("eps_out", eps_out, lat_shape, f32)
         _check(lib().synerdiff_unet_step(self.h, n, _ptr(latents), _ptr(ts), _ptr(cf), _ptr(gd), _ptr(ctx_cond),
                                          _ptr(ctx_uncond), _ptr(pooled_cond), _ptr(pooled_uncond), _ptr(ti),
                                          _ptr(cc), _ptr(out), _ptr(eps_out), self._stream(stream)))
         return out
+
+    def _check_dev(self, name, t, shape, dtype):
+        """A device tensor the C ABI reads or writes through a raw pointer:
+        the library cannot see its size, so shape, dtype, device and layout
+        are checked here before the call."""
+        torch = self.torch
+        if not isinstance(t, torch.Tensor):
+            raise ValueError(f"{name}: expected a torch tensor, got {type(t).__name__}")
+        if t.device.type != self.device.type or (self.device.index is not None and t.device.index != self.device.index):
+            raise ValueError(f"{name}: must live on {self.device}, got {t.device}")
+        if t.dtype != dtype:
+            raise ValueError(f"{name}: dtype {t.dtype}, expected {dtype}")
+        if tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name}: must be contiguous")
+
+    @staticmethod
+    def _host(name, a, dtype, shape):
+        """A host array the C ABI reads n entries of: converted to a
+        contiguous array of `dtype` and checked against `shape`."""
+        if a is None:
+            raise ValueError(f"{name}: required")
+        if hasattr(a, "device") and getattr(a.device, "type", "cpu") != "cpu":
+            raise ValueError(f"{name}: must be a host array")
+        arr = np.ascontiguousarray(np.asarray(a), dtype)
+        if arr.shape != tuple(shape):
+            raise ValueError(f"{name}: shape {arr.shape}, expected {tuple(shape)}")
+        return arr
 
     def profile(self, enable=True):
         _check(lib().synerdiff_profile(self.h, int(enable)))

@@ -8,6 +8,8 @@
 namespace sd {
 
 enum DType { F32 = 0, BF16 = 1 };
+// bf16 storage as seen from host code (the kernels read it as __bf16).
+typedef uint16_t bf16_t;
 
 // One K-segment of an implicit-GEMM A operand.  Row m of A is output pixel
 // (img, oy, ox) of an Ho x Wo image; column k is (tap, c) with
@@ -141,6 +143,28 @@ hipError_t launch_linear_smallm(DType wdt, const float* in, int M, int K, const 
 // Rows dst0 .. dst0 + n - 1 of a row-major tensor (row_bytes each, a
 // multiple of 16) become copies of rows src_rows[0 .. n - 1].
 hipError_t launch_copy_rows(void* base, long row_bytes, int dst0, int n, const int* src_rows, hipStream_t s);
+// Output conv (3x3, C -> 4) of each request's rows + CFG combine + DDIM in
+// one kernel (bf16): x holds the normalised (GroupNorm + SiLU) rows
+// [rows, H, W, C]; w the conv weight packed [4][9 C] (tap-major, channel-
+// minor), bias [4].  Request r reads row r and, if req_row_u[r] >= 0, that
+// unconditional row; lat_* are [n_req, 4, H, W] fp32.  order (or null)
+// lists the requests in launch order.
+struct OutArgs {
+  const bf16_t* x;
+  const bf16_t* w;
+  const float* bias;
+  const float* lat_in;
+  float* lat_out;
+  float* eps_out;  // or null
+  const int* req_row_u;
+  const float* req_coef;  // [n_req, 3] = (A, B, w)
+  const int* order;
+  int n_req, H, W, C;
+  int tiles;  // set by the launcher
+};
+bool out_cfg_ddim_ok(DType dt, int latent_c, int H, int W, int C);
+size_t out_cfg_ddim_lds_bytes(int W);
+hipError_t launch_out_cfg_ddim(const OutArgs& a, hipStream_t s);
 hipError_t launch_cfg_ddim(const float* eps_rows, const float* lat_in, float* lat_out,
                            float* eps_out, int n_req, int lc, int hw, const int* req_row_u,
                            const float* req_coef, hipStream_t s);

@@ -159,6 +159,21 @@ sd_status synerdiff_op_groupnorm_stats(int32_t dtype, const void* x0, int32_t c0
                 "groupnorm");
 }
 
+sd_status synerdiff_op_groupnorm_fused(int32_t dtype, const void* x0, int32_t c0, const void* x1, int32_t c1,
+                                       int32_t n, int32_t hw, int32_t groups, float eps, const float* gamma,
+                                       const float* beta, int32_t silu, void* out, void* stream) {
+  if (dtype != SD_BF16) return op_fail(SD_ERR_UNSUPPORTED, "the one-kernel GroupNorm is bf16 only");
+  const int cin = c0 + c1;
+  if (n < 0 || hw < 1 || c0 < 4 || c1 < 0 || groups < 1 || cin % groups) return op_fail(SD_ERR_INVALID_ARG, "bad shape");
+  if (!groupnorm_fused_ok(BF16, c0, c1, hw, groups) || n > 65535)
+    return op_fail(SD_ERR_UNSUPPORTED, "shape outside the one-kernel GroupNorm's range");
+  if (n == 0) return SD_OK;
+  if (!x0 || (c1 && !x1) || !gamma || !beta || !out) return op_fail(SD_ERR_INVALID_ARG, "NULL argument");
+  return op_hip(launch_groupnorm_fused(BF16, x0, c0, x1, c1, n, hw, groups, eps, gamma, beta, silu ? 1 : 0, out,
+                                       (hipStream_t)stream),
+                "groupnorm_fused");
+}
+
 sd_status synerdiff_op_layernorm(int32_t dtype, const void* x, void* y, int64_t tokens, int32_t C,
                                  const float* gamma, const float* beta, float eps, void* stream) {
   if (bad_dtype(dtype)) return op_fail(SD_ERR_INVALID_ARG, "bad dtype");
@@ -197,6 +212,42 @@ sd_status synerdiff_op_geglu(int32_t dtype, const void* x, void* y, int64_t toke
   if (!x || !y) return op_fail(SD_ERR_INVALID_ARG, "NULL argument");
   if (tokens < 0 || half < 8 || half % 8) return op_fail(SD_ERR_INVALID_ARG, "bad shape");
   return op_hip(launch_geglu((DType)dtype, x, y, tokens, half, (hipStream_t)stream), "geglu");
+}
+
+sd_status synerdiff_op_conv_out_cfg_ddim(int32_t dtype, const void* x, int32_t H, int32_t W, int32_t C,
+                                         const void* w, const float* bias, int32_t n_req, const int32_t* req_row_u,
+                                         const float* req_coef, const float* lat_in, float* lat_out, float* eps_out,
+                                         void* stream) {
+  if (dtype != SD_BF16) return op_fail(SD_ERR_UNSUPPORTED, "the fused output kernel is bf16 only");
+  if (n_req < 0 || H < 1 || W < 1) return op_fail(SD_ERR_INVALID_ARG, "bad shape");
+  if (!out_cfg_ddim_ok(BF16, 4, H, W, C)) return op_fail(SD_ERR_UNSUPPORTED, "unsupported shape (C % 32, C <= 320, W <= 128)");
+  if (n_req == 0) return SD_OK;
+  if (!x || !w || !bias || !req_row_u || !req_coef || !lat_in || !lat_out)
+    return op_fail(SD_ERR_INVALID_ARG, "NULL argument");
+  const size_t lat = (size_t)n_req * 4 * H * W * 4;
+  const auto overlap = [](const void* a, const void* b, size_t n) {
+    const uint8_t *pa = (const uint8_t*)a, *pb = (const uint8_t*)b;
+    return pa < pb + n && pb < pa + n;
+  };
+  if (lat_out != lat_in && overlap(lat_out, lat_in, lat)) return op_fail(SD_ERR_INVALID_ARG, "latents overlap");
+  if (eps_out && (overlap(eps_out, lat_in, lat) || overlap(eps_out, lat_out, lat)))
+    return op_fail(SD_ERR_INVALID_ARG, "eps_out overlaps the latents");
+  OutArgs a;
+  memset(&a, 0, sizeof(a));
+  a.x = (const bf16_t*)x;
+  a.w = (const bf16_t*)w;
+  a.bias = bias;
+  a.lat_in = lat_in;
+  a.lat_out = lat_out;
+  a.eps_out = eps_out;
+  a.req_row_u = req_row_u;
+  a.req_coef = req_coef;
+  a.order = nullptr;
+  a.n_req = n_req;
+  a.H = H;
+  a.W = W;
+  a.C = C;
+  return op_hip(launch_out_cfg_ddim(a, (hipStream_t)stream), "conv_out_cfg_ddim");
 }
 
 }  // extern "C"

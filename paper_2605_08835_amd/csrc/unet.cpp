@@ -363,9 +363,9 @@ static void build_layout(sd_unet* h) {
 }
 
 // ------------------------------------------------------------- profiling
-enum Kind { K_GEMM, K_ATTN, K_GN, K_LN, K_GEGLU, K_TIME, K_PACK, K_CFG, K_COPY, K_COUNT };
+enum Kind { K_GEMM, K_ATTN, K_GN, K_LN, K_GEGLU, K_TIME, K_PACK, K_CFG, K_COPY, K_OUT, K_COUNT };
 static const char* kKindName[K_COUNT] = {"gemm", "attention", "groupnorm", "layernorm", "geglu",
-                                         "time_mlp", "pack", "cfg_ddim", "copy"};
+                                         "time_mlp", "pack", "cfg_ddim", "copy", "out_cfg_ddim"};
 
 static hipEvent_t take_event(sd_unet* h) {
   if (!h->pool.empty()) {
@@ -743,6 +743,7 @@ struct Step {
     const int* req_row_u = (const int*)(scal + 4 * (8 * R));
     const float* req_coef = (const float*)(scal + 4 * (9 * R));
     const float* time_ids = (const float*)(scal + 4 * (12 * R));
+    const int* req_order = (const int*)(scal + 4 * (12 * R + 64));
 
     if (!dry && h->prof) prof_mark(h, -1, nullptr, 0, 0, s);
     // contexts: [cond_0 .. cond_{n-1}, uncond]
@@ -880,8 +881,31 @@ struct Step {
         Wd *= 2;
       }
     }
-    // output: GN + SiLU + conv (fp32 eps rows), then CFG combine + DDIM
+    // output: GN + SiLU, then the output conv, CFG combine and DDIM in one
+    // kernel (bf16) or as conv (fp32 eps rows) + combine
     void* no = gn_norm(cur, curc, nullptr, 0, H * Wd, 1e-5f, h->outg, h->outb, 1);
+    if (out_cfg_ddim_ok(h->dt, c.latent_c, H, Wd, curc)) {
+      if (dry || err) return;
+      OutArgs oa;
+      memset(&oa, 0, sizeof(oa));
+      oa.x = (const bf16_t*)no;
+      oa.w = (const bf16_t*)W(h->conv_out.w);
+      oa.bias = Wf(h->conv_out.b);
+      oa.lat_in = lat_in;
+      oa.lat_out = lat_out;
+      oa.eps_out = eps_out;
+      oa.req_row_u = req_row_u;
+      oa.req_coef = req_coef;
+      oa.order = req_order;
+      oa.n_req = n_req;
+      oa.H = H;
+      oa.W = Wd;
+      oa.C = curc;
+      const double hw = (double)H * Wd;
+      ok(launch_out_cfg_ddim(oa, s), "conv_out+cfg+ddim", K_OUT, 2.0 * rows * hw * 9.0 * curc * c.latent_c,
+         (double)rows * hw * curc * h->esz + 4.0 * c.latent_c * hw * n_req * (2.0 + (eps_out ? 1.0 : 0.0)));
+      return;
+    }
     float* eps = (float*)buf(R_EPS, (size_t)rows * H * Wd * c.latent_c * 4);
     Epi eo = epi(eps, c.latent_c, Wf(h->conv_out.b));
     eo.out_f32 = 1;
@@ -896,7 +920,7 @@ struct Step {
 
 static void plan_workspace(sd_unet* h) {
   const int R = h->cfg.max_requests;
-  h->scal_bytes = (size_t)4 * (12 * R + 64);
+  h->scal_bytes = (size_t)4 * (13 * R + 64);
   Step st{h, true, nullptr, R, 2 * R};
   st.run(nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
   size_t o = 0;
@@ -1330,6 +1354,7 @@ sd_status synerdiff_unet_step(sd_unet* h, int32_t n_req, const float* lat_in, co
   int32_t* req_row_u = (int32_t*)(p + 4 * (8 * R));
   float* req_coef = (float*)(p + 4 * (9 * R));
   float* tid = (float*)(p + 4 * (12 * R));
+  int32_t* req_order = (int32_t*)(p + 4 * (12 * R + 64));
   int rows = 0;
   synerdiff_row_plan(n_req, cfg_on, row_req, row_branch, req_row_u, &rows);
   for (int i = 0; i < rows; ++i) {
@@ -1342,6 +1367,13 @@ sd_status synerdiff_unet_step(sd_unet* h, int32_t n_req, const float* lat_in, co
     req_coef[3 * r + 2] = cfg_on[r] ? guidance[r] : 1.0f;
   }
   for (int i = 0; i < c.n_time_ids && time_ids; ++i) tid[i] = time_ids[i];
+  {  // requests with two rows (the longer output blocks) are launched first
+    int k = 0;
+    for (int r = 0; r < n_req; ++r)
+      if (cfg_on[r]) req_order[k++] = r;
+    for (int r = 0; r < n_req; ++r)
+      if (!cfg_on[r]) req_order[k++] = r;
+  }
   if (hipMemcpyAsync(h->ws + h->off.at(R_SCAL), p, h->scal_bytes, hipMemcpyHostToDevice, s) != hipSuccess ||
       hipEventRecord(h->ev[slot], s) != hipSuccess)
     return fail(SD_ERR_HIP, "scalar upload failed");

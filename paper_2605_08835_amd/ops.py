@@ -93,3 +93,27 @@ def geglu(x):
     y = torch.empty(x.shape[:-1] + (half,), device=x.device, dtype=x.dtype)
     _check(lib().synerdiff_op_geglu(_dt(x), _ptr(x), _ptr(y), x.numel() // x.shape[-1], half, _s()))
     return y
+
+
+def conv_out_cfg_ddim(x, w_packed, bias, req_row_u, req_coef, lat_in, lat_out=None, eps_out=None):
+    """Output conv (3x3, C -> 4) + CFG combine + DDIM; x [rows, H, W, C] bf16,
+    req_row_u int32 [n_req] and req_coef fp32 [n_req, 3] on the device."""
+    n, H, W, C = x.shape
+    n_req = int(req_row_u.shape[0])
+    if lat_out is None:
+        lat_out = torch.empty_like(lat_in)
+    _check(lib().synerdiff_op_conv_out_cfg_ddim(_dt(x), _ptr(x), H, W, C, _ptr(w_packed), _ptr(bias), n_req,
+                                                _ptr(req_row_u), _ptr(req_coef), _ptr(lat_in), _ptr(lat_out),
+                                                _ptr(eps_out), _s()))
+    return lat_out
+
+
+def groupnorm_fused(x0, groups, eps, gamma, beta, x1=None, silu=True):
+    """GroupNorm (+ SiLU) of [x0 | x1] in one kernel (bf16, small images)."""
+    n, H, W, c0 = x0.shape
+    c1 = 0 if x1 is None else x1.shape[3]
+    out = torch.empty(n, H, W, c0 + c1, device=x0.device, dtype=x0.dtype)
+    _check(lib().synerdiff_op_groupnorm_fused(_dt(x0), _ptr(x0), c0, _ptr(x1), c1, n, H * W, groups, float(eps),
+                                              _ptr(gamma), _ptr(beta), int(silu), _ptr(out), _s()))
+    return out
+

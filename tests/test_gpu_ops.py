@@ -357,3 +357,108 @@ def test_conv_large_grid_rows_independent(ops):
     full = ops.conv(_dev(x, "bf16"), wp, 160)[:3].float().cpu().numpy()
     part = ops.conv(_dev(x[:3], "bf16"), wp, 160).float().cpu().numpy()
     assert np.array_equal(full, part)
+
+
+OUT_CASES = [
+    # n_req, cfg flags, H, W, C, in place, eps_out
+    (3, (1, 0, 1), 12, 10, 64, False, True),     # one ragged tile (120 pixels)
+    (5, (0, 1, 1, 0, 1), 16, 16, 320, False, True),
+    (2, (1, 1), 64, 64, 320, True, True),       # 16 tiles, halo rows across tiles
+    (2, (1, 0), 20, 20, 96, False, False),      # 3 MFMA steps, ragged last tile
+    (1, (1,), 8, 128, 32, False, True),         # widest rows (LDS above 64 KB)
+    (2, (0, 0), 1, 5, 32, False, True),         # one image row
+    (4, (1, 0, 0, 1), 33, 7, 160, True, False),
+]
+
+
+@pytest.mark.parametrize("case", OUT_CASES)
+def test_conv_out_cfg_ddim(ops, case):
+    """The fused output kernel against the oracle's conv2d, CFG combine and
+    DDIM update (x' = A x + B eps with the same A, B) per request."""
+    from oracle.sampler import cfg_combine
+    n_req, cfg, H, W, C, inplace, want_eps = case
+    rng = np.random.default_rng(1000 + H * W + C)
+    cfg = np.array(cfg, np.int32)
+    n_rows = n_req + int(cfg.sum())
+    ru = np.full(n_req, -1, np.int32)
+    ru[cfg == 1] = n_req + np.arange(int(cfg.sum()))
+    x = _vals(rng, (n_rows, H, W, C), "bf16")
+    w = _vals(rng, (4, C, 3, 3), "bf16", 0.05)
+    b = (rng.standard_normal(4) * 0.1).astype(np.float32)
+    coef = np.stack([rng.uniform(0.9, 1.3, n_req), rng.uniform(-0.3, 0.0, n_req),
+                     rng.uniform(5.0, 9.0, n_req)], 1).astype(np.float32)
+    lat = rng.standard_normal((n_req, 4, H, W)).astype(np.float32)
+    lat_in = _dev(lat)
+    lat_out = lat_in if inplace else torch.empty_like(lat_in)
+    eps_out = torch.empty_like(lat_in) if want_eps else None
+    ops.conv_out_cfg_ddim(_dev(x, "bf16"), _dev(_pack(w), "bf16"), _dev(b), _dev(ru), _dev(coef), lat_in,
+                          lat_out, eps_out)
+    torch.cuda.synchronize()
+    got = lat_out.cpu().double().numpy()
+    got_e = eps_out.cpu().double().numpy() if want_eps else None
+    for r in range(n_req):
+        ec = O.conv2d(x[r].astype(np.float64), w, b)
+        e = cfg_combine(ec, O.conv2d(x[ru[r]].astype(np.float64), w, b), float(coef[r, 2])) if ru[r] >= 0 else ec
+        e = e.transpose(2, 0, 1)  # (4, H, W)
+        ref = float(coef[r, 0]) * lat[r].astype(np.float64) + float(coef[r, 1]) * e
+        err = rel_l2(got[r], ref)
+        log(f"  out+cfg+ddim {case} request {r}: rel L2 latents {err:.2e}")
+        assert err <= 1e-5, (r, err)
+        if want_eps:
+            assert rel_l2(got_e[r], e) <= 1e-5, r
+
+
+def test_conv_out_cfg_ddim_rejects_unsupported(ops):
+    from paper_2605_08835_amd.binding import SynerDiffError
+    x = torch.zeros(2, 4, 4, 48, device="cuda", dtype=torch.bfloat16)   # C % 32 != 0
+    w = torch.zeros(4, 9 * 48, device="cuda", dtype=torch.bfloat16)
+    ru = torch.tensor([-1, -1], device="cuda", dtype=torch.int32)
+    coef = torch.ones(2, 3, device="cuda")
+    lat = torch.zeros(2, 4, 4, 4, device="cuda")
+    with pytest.raises(SynerDiffError):
+        ops.conv_out_cfg_ddim(x, w, torch.zeros(4, device="cuda"), ru, coef, lat)
+
+
+GN_FUSED_CASES = [
+    # n, H, W, c0, c1, groups, silu  (variant: vectors per thread x channels per load)
+    (3, 8, 8, 1280, 0, 32, 1),      # 4 x 8
+    (2, 16, 16, 1280, 0, 32, 1),    # 8 x 8
+    (2, 16, 16, 2560, 0, 32, 1),    # 10 x 8
+    (2, 16, 16, 1280, 640, 32, 1),  # 20 x 4 (a group straddles the two sources)
+    (2, 16, 16, 64, 32, 8, 0),      # 4 x 4, 12 channels per group, no SiLU
+    (3, 16, 16, 640, 0, 32, 1),     # 8 x 4
+    (2, 8, 8, 2560, 0, 32, 0),      # 4 x 8
+    (1, 3, 5, 320, 320, 32, 1),     # ragged image
+]
+
+
+@pytest.mark.parametrize("case", GN_FUSED_CASES)
+def test_groupnorm_fused(ops, case):
+    """The one-kernel GroupNorm + SiLU of the small levels against the
+    oracle's group_norm (and silu), per image."""
+    n, H, W, c0, c1, G, silu = case
+    rng = np.random.default_rng(7 * c0 + c1 + H)
+    x0 = bf16_round(_vals(rng, (n, H, W, c0), "bf16", 2.0) + np.float32(0.5))
+    x1 = _vals(rng, (n, H, W, c1), "bf16") if c1 else None
+    g = (1 + 0.1 * rng.standard_normal(c0 + c1)).astype(np.float32)
+    b = (0.1 * rng.standard_normal(c0 + c1)).astype(np.float32)
+    y = ops.groupnorm_fused(_dev(x0, "bf16"), G, 1e-5, _dev(g), _dev(b), x1=_dev(x1, "bf16") if c1 else None,
+                            silu=bool(silu))
+    torch.cuda.synchronize()
+    y = y.float().cpu().numpy().astype(np.float64)
+    for i in range(n):
+        a = x0[i].astype(np.float64) if not c1 else np.concatenate([x0[i], x1[i]], axis=2).astype(np.float64)
+        ref = O.group_norm(a, G, g, b, 1e-5)
+        if silu:
+            ref = O.silu(ref)
+        err = rel_l2(y[i], ref)
+        log(f"  groupnorm fused {case} image {i}: rel L2 {err:.2e}")
+        assert err <= 6e-3, (i, err)  # one bf16 rounding of the output
+
+
+def test_groupnorm_fused_rejects_large_images(ops):
+    from paper_2605_08835_amd.binding import SynerDiffError
+    x = torch.zeros(1, 64, 64, 320, device="cuda", dtype=torch.bfloat16)
+    g = torch.ones(320, device="cuda")
+    with pytest.raises(SynerDiffError):
+        ops.groupnorm_fused(x, 32, 1e-5, g, g)

@@ -139,8 +139,11 @@ def test_in_place_and_empty_batch(weights_cache):
     a, _ = gpu_step(m, req)
     b, _ = gpu_step(m, req, out_inplace=True)
     assert np.array_equal(a, b)
+    u = get_config(wl)["unet"]
     lat = torch.zeros(0, 4, 12, 12, device="cuda")
-    m.step(lat, np.zeros(0, np.int32), np.zeros(0, np.uint8), np.zeros(0, np.float32), lat, lat,
+    ctx = torch.zeros(0, u["ctx_len"], u["ctx_dim"], device="cuda", dtype=m.act_dtype)
+    unc = torch.zeros(u["ctx_len"], u["ctx_dim"], device="cuda", dtype=m.act_dtype)
+    m.step(lat, np.zeros(0, np.int32), np.zeros(0, np.uint8), np.zeros(0, np.float32), ctx, unc,
            np.zeros((0, 2), np.float32), out=lat)
 
 
