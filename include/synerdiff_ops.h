@@ -87,6 +87,24 @@ sd_status synerdiff_op_groupnorm_stats(int32_t dtype, const void* d_x0, int32_t 
                                        const float* d_gamma, const float* d_beta, float* d_partial,
                                        float* d_scale, float* d_shift, void* hip_stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * synerdiff_op_groupnorm_stats without d_partial.  The partial sums go to a
+ * device array the library owns, SYNERDIFF_GN_NOALLOC_SCRATCH_FLOATS floats
+ * (16 MiB) per device, held until the process ends; the call itself
+ * allocates nothing.  A call whose partial sums,
+ * synerdiff_op_groupnorm_scratch_floats(n, hw, c0 + c1), exceed that size
+ * returns SD_ERR_CAPACITY before enqueueing anything.  Every call on a device
+ * shares its array: calls that overlap in time on one device (different
+ * streams or host threads) race.  Each call writes every partial it reads,
+ * so no clearing is needed between calls.  Arguments and outputs as for
+ * synerdiff_op_groupnorm_stats. */
+#define SYNERDIFF_GN_NOALLOC_SCRATCH_FLOATS (1u << 22)
+sd_status synerdiff_op_groupnorm_stats_noalloc(int32_t dtype, const void* d_x0, int32_t c0, const void* d_x1,
+                                               int32_t c1, int32_t n, int32_t hw, int32_t groups, float eps,
+                                               const float* d_gamma, const float* d_beta, float* d_scale,
+                                               float* d_shift, void* hip_stream);
+
 /* GroupNorm of the concat [x0 | x1] ([n, hw, c0 + c1], `groups` groups of
  * consecutive channels, biased variance, eps) followed by SiLU when silu =
  * 1, written to out [n, hw, c0 + c1]: the normalisation in front of every

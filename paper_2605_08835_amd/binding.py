@@ -81,6 +81,8 @@ _SIG = {
     "synerdiff_op_conv_out_cfg_ddim": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, ctypes.c_int32,
                                                       ctypes.c_int32, _P, _P, ctypes.c_int32, _P, _P, _P, _P, _P,
                                                       _P]),
+    "synerdiff_op_groupnorm_stats_noalloc": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, _P] +
+                                             [ctypes.c_int32] * 4 + [ctypes.c_float, _P, _P, _P, _P, _P]),
     "synerdiff_op_groupnorm_fused": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, _P] + [ctypes.c_int32] * 4 +
                                      [ctypes.c_float, _P, _P, ctypes.c_int32, _P, _P]),
     "synerdiff_op_layernorm": (ctypes.c_int, [ctypes.c_int32, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P,

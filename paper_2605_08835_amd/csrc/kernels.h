@@ -98,6 +98,11 @@ hipError_t launch_groupnorm_stats(DType dt, const void* src0, int c0, const void
                                   const float* beta, float* partial, float* scale, float* shift,
                                   hipStream_t s);
 size_t groupnorm_partial_floats(int imgs, int hw, int cin);
+// The library's own partial-sum array on the current device (a static
+// __device__ array of groupnorm_scratch_floats_max() floats; its address is
+// looked up once per device) for the entry point that allocates nothing.
+size_t groupnorm_scratch_floats_max();
+hipError_t groupnorm_scratch(float** out);
 // out = act(x * scale + shift) over the concat [src0 | src1] (act = SiLU or identity).
 // Statistics and apply in one launch for small images (bf16; see
 // groupnorm_fused_ok for the shapes it takes).

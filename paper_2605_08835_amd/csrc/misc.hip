@@ -1,6 +1,9 @@
 // Memory-bound kernels of the step: row packing, time-embedding inputs and
 // small-M MLP, GroupNorm statistics, LayerNorm, GEGLU and the fused CFG
 // combine + DDIM update.
+#include <map>
+#include <mutex>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -350,6 +353,39 @@ hipError_t launch_groupnorm_stats(DType dt, const void* src0, int c0, const void
   gn_finalize_kernel<<<dim3(groups, imgs), 64, 0, s>>>(partial, cin, nsplit, hw, groups, eps, gamma, beta,
                                                        scale, shift);
   return hipGetLastError();
+}
+
+// Library-owned scratch for the GroupNorm partial sums of callers that
+// cannot allocate device memory (synerdiff_op_groupnorm_stats_noalloc):
+// one array per device, held until the process ends.  In host code the name
+// `gn_scratch` stands for a host-side shadow, not a device address, so host
+// code never passes it to a kernel: it takes the device address from
+// hipGetSymbolAddress, once per device (with that device current), and uses
+// that pointer everywhere.  The partial-sum kernel writes every element the
+// finalize kernel reads, so nothing needs clearing between calls; calls
+// that overlap in time on one device share the array and race.
+constexpr size_t GN_SCRATCH_FLOATS = (size_t)1 << 22;  // 16 MiB
+static __device__ __align__(256) float gn_scratch[GN_SCRATCH_FLOATS];
+
+size_t groupnorm_scratch_floats_max() { return GN_SCRATCH_FLOATS; }
+
+hipError_t groupnorm_scratch(float** out) {
+  static std::mutex mu;
+  static std::map<int, float*> by_device;
+  *out = nullptr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = by_device.find(dev);
+  if (it == by_device.end()) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(gn_scratch));
+    if (e != hipSuccess) return e;
+    it = by_device.emplace(dev, static_cast<float*>(p)).first;
+  }
+  *out = it->second;
+  return hipSuccess;
 }
 
 // Pass 3: y = act(x * scale + shift) into a materialised [imgs, hw, cin]

@@ -159,6 +159,30 @@ sd_status synerdiff_op_groupnorm_stats(int32_t dtype, const void* x0, int32_t c0
                 "groupnorm");
 }
 
+sd_status synerdiff_op_groupnorm_stats_noalloc(int32_t dtype, const void* x0, int32_t c0, const void* x1, int32_t c1,
+                                               int32_t n, int32_t hw, int32_t groups, float eps, const float* gamma,
+                                               const float* beta, float* scale, float* shift, void* stream) {
+  if (bad_dtype(dtype)) return op_fail(SD_ERR_INVALID_ARG, "bad dtype");
+  if (!x0 || (c1 && !x1) || !gamma || !beta || !scale || !shift) return op_fail(SD_ERR_INVALID_ARG, "NULL argument");
+  const int cin = c0 + c1;
+  if (n < 0 || hw < 1 || c0 < 8 || c0 % 8 || c1 < 0 || c1 % 8 || groups < 1 || cin % groups)
+    return op_fail(SD_ERR_INVALID_ARG, "bad shape");
+  if (cin > 4096) return op_fail(SD_ERR_UNSUPPORTED, "too many channels");
+  if (n == 0) return SD_OK;
+  const size_t need = groupnorm_partial_floats(n, hw, cin);
+  if (need > groupnorm_scratch_floats_max()) {
+    g_err = "groupnorm_stats_noalloc: " + std::to_string(need) + " partial floats exceed the library scratch of " +
+            std::to_string(groupnorm_scratch_floats_max()) + " (use synerdiff_op_groupnorm_stats with a buffer)";
+    return SD_ERR_CAPACITY;
+  }
+  float* part = nullptr;
+  const sd_status st = op_hip(groupnorm_scratch(&part), "groupnorm scratch address");
+  if (st != SD_OK) return st;
+  return op_hip(launch_groupnorm_stats((DType)dtype, x0, c0, x1, c1, n, hw, groups, eps, gamma, beta, part, scale,
+                                       shift, (hipStream_t)stream),
+                "groupnorm_noalloc");
+}
+
 sd_status synerdiff_op_groupnorm_fused(int32_t dtype, const void* x0, int32_t c0, const void* x1, int32_t c1,
                                        int32_t n, int32_t hw, int32_t groups, float eps, const float* gamma,
                                        const float* beta, int32_t silu, void* out, void* stream) {

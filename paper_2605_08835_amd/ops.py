@@ -117,3 +117,16 @@ def groupnorm_fused(x0, groups, eps, gamma, beta, x1=None, silu=True):
                                               _ptr(gamma), _ptr(beta), int(silu), _ptr(out), _s()))
     return out
 
+
+def groupnorm_stats_noalloc(x0, groups, eps, gamma, beta, x1=None, scale=None, shift=None):
+    """GroupNorm statistics through the entry point that allocates nothing
+    (the partial sums live in the library's own device array)."""
+    n, H, W, c0 = x0.shape
+    c1 = 0 if x1 is None else x1.shape[3]
+    cin = c0 + c1
+    scale = torch.empty(n, cin, device=x0.device) if scale is None else scale
+    shift = torch.empty(n, cin, device=x0.device) if shift is None else shift
+    _check(lib().synerdiff_op_groupnorm_stats_noalloc(_dt(x0), _ptr(x0), c0, _ptr(x1), c1, n, H * W, groups,
+                                                      float(eps), _ptr(gamma), _ptr(beta), _ptr(scale),
+                                                      _ptr(shift), _s()))
+    return scale, shift
