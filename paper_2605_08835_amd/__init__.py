@@ -7,4 +7,5 @@ streams.  Importing the package does not load the library; the first call
 that needs it does, and raises if it is missing.
 """
 from .binding import (UNet, UNetConfig, alphas_cumprod, config_from_dict, ddim_coef,  # noqa: F401
-                      lib, manifest, row_plan, SynerDiffError)
+                      lib, manifest, row_plan, SynerDiffError, VAE, VAEConfig, vae_config_from_dict, vae_manifest,
+                      vae_chunk_plan, chunk_cost, plan_sequence)

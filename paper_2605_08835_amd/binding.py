@@ -42,6 +42,13 @@ class LayerStat(ctypes.Structure):
                 ("flop", ctypes.c_double), ("bytes", ctypes.c_double)]
 
 
+class VAEConfig(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("latent_c", "latent_h", "latent_w", "n_levels")] + \
+               [("ch", ctypes.c_int32 * 4)] + \
+               [(n, ctypes.c_int32) for n in ("n_res", "gn_groups", "out_c", "max_images", "dtype")] + \
+               [("scaling", ctypes.c_float)]
+
+
 _P = ctypes.c_void_p
 _SIG = {
     "synerdiff_abi_version": (ctypes.c_int32, []),
@@ -67,6 +74,30 @@ _SIG = {
                                               ctypes.POINTER(ctypes.c_int32), ctypes.c_int32]),
     "synerdiff_profile_read_layers": (ctypes.c_int, [_P, ctypes.POINTER(LayerStat), ctypes.c_int32,
                                                      ctypes.POINTER(ctypes.c_int32), ctypes.c_int32]),
+    "synerdiff_vae_config_check": (ctypes.c_int, [ctypes.POINTER(VAEConfig)]),
+    "synerdiff_vae_param_count": (ctypes.c_int64, [ctypes.POINTER(VAEConfig)]),
+    "synerdiff_vae_param_info": (ctypes.c_int, [ctypes.POINTER(VAEConfig), ctypes.c_int64, ctypes.c_char_p,
+                                                ctypes.c_size_t, ctypes.POINTER(ctypes.c_int64),
+                                                ctypes.POINTER(ctypes.c_int32)]),
+    "synerdiff_vae_weights_bytes": (ctypes.c_size_t, [ctypes.POINTER(VAEConfig)]),
+    "synerdiff_vae_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(VAEConfig)]),
+    "synerdiff_vae_create": (ctypes.c_int, [ctypes.POINTER(VAEConfig), _P, ctypes.c_size_t, _P, ctypes.c_size_t,
+                                            ctypes.POINTER(_P)]),
+    "synerdiff_vae_load_weights": (ctypes.c_int, [_P, _P, ctypes.c_size_t, _P]),
+    "synerdiff_vae_stage_count": (ctypes.c_int32, [_P]),
+    "synerdiff_vae_stage_name": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_char_p, ctypes.c_size_t]),
+    "synerdiff_vae_stage_flops": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_double)]),
+    "synerdiff_vae_run": (ctypes.c_int, [_P, ctypes.c_int32, _P, ctypes.c_int32, ctypes.c_int32, _P, _P]),
+    "synerdiff_vae_destroy": (None, [_P]),
+    "synerdiff_vae_activation": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64)] +
+                                 [ctypes.POINTER(ctypes.c_int32)] * 3),
+    "synerdiff_vae_chunk_plan": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _P]),
+    "synerdiff_chunk_cost": (ctypes.c_int, [_P, _P, ctypes.c_int32, ctypes.c_double, ctypes.c_double,
+                                            ctypes.c_double, ctypes.POINTER(ctypes.c_double),
+                                            ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
+    "synerdiff_plan_sequence": (ctypes.c_int, [ctypes.c_int32] * 4 + [_P, _P, ctypes.c_double, ctypes.c_int32,
+                                               ctypes.c_int32, _P, ctypes.POINTER(ctypes.c_int32),
+                                               ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
     "synerdiff_op_conv": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, _P] + [ctypes.c_int32] * 7 +
                           [_P, _P, ctypes.c_int32, _P, ctypes.c_int32, _P, _P, _P, ctypes.c_int32, _P,
                            ctypes.c_int64, _P]),
@@ -329,3 +360,162 @@ class UNet:
 
 def _align(p):
     return (p + 255) & ~255
+
+
+def vae_config_from_dict(vae, max_images):
+    c = VAEConfig()
+    c.latent_c, c.latent_h, c.latent_w = vae["latent_c"], vae["latent_h"], vae["latent_w"]
+    c.n_levels = len(vae["ch"])
+    for i, v in enumerate(vae["ch"]):
+        c.ch[i] = v
+    c.n_res, c.gn_groups, c.out_c = vae["n_res"], vae["gn_groups"], vae["out_c"]
+    c.max_images = max_images
+    c.dtype = SD_BF16 if vae["dtype"] == "bf16" else SD_F32
+    c.scaling = vae["scaling"]
+    return c
+
+
+def vae_manifest(cfg):
+    """[(name, shape)] of the decoder parameters the library expects, in load order."""
+    L = lib()
+    n = L.synerdiff_vae_param_count(ctypes.byref(cfg))
+    if n < 0:
+        raise SynerDiffError(-2, L.synerdiff_last_error().decode())
+    out = []
+    name = ctypes.create_string_buffer(256)
+    shape = (ctypes.c_int64 * 4)()
+    nd = ctypes.c_int32()
+    for i in range(n):
+        _check(L.synerdiff_vae_param_info(ctypes.byref(cfg), i, name, 256, shape, ctypes.byref(nd)))
+        out.append((name.value.decode(), tuple(shape[k] for k in range(nd.value))))
+    return out
+
+
+def vae_chunk_plan(stage_cost, c):
+    """Boundaries b_0 = 0 < ... < b_c = len(stage_cost) of the c contiguous
+    chunks with the smallest largest-chunk cost."""
+    cost = np.ascontiguousarray(stage_cost, np.float64)
+    out = np.zeros(c + 1, np.int32)
+    _check(lib().synerdiff_vae_chunk_plan(_ptr(cost), len(cost), int(c), _ptr(out)))
+    return [int(x) for x in out]
+
+
+def chunk_cost(t_u, t_v, T_u0, T_v0, lam):
+    """Eq. (2) cumulative latencies and the Eq. (1) cost: (T_u(c), T_v(c), L(c))."""
+    tu = np.ascontiguousarray(t_u, np.float64)
+    tv = np.ascontiguousarray(t_v, np.float64)
+    a, b, l = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    _check(lib().synerdiff_chunk_cost(_ptr(tu), _ptr(tv), len(tu), float(T_u0), float(T_v0), float(lam),
+                                      ctypes.byref(a), ctypes.byref(b), ctypes.byref(l)))
+    return a.value, b.value, l.value
+
+
+class VAE:
+    """One VAE-decoder handle over torch-allocated device buffers."""
+
+    def __init__(self, vae, max_images, device=None):
+        import torch
+        self.torch = torch
+        self.vae = vae
+        self.cfg = vae_config_from_dict(vae, max_images)
+        L = lib()
+        _check(L.synerdiff_vae_config_check(ctypes.byref(self.cfg)))
+        self.device = torch.device(device or "cuda")
+        wb = L.synerdiff_vae_weights_bytes(ctypes.byref(self.cfg))
+        wsb = L.synerdiff_vae_workspace_bytes(ctypes.byref(self.cfg))
+        self.wbuf = torch.empty(wb + 256, dtype=torch.uint8, device=self.device)
+        self.ws = torch.empty(wsb + 256, dtype=torch.uint8, device=self.device)
+        h = ctypes.c_void_p()
+        _check(L.synerdiff_vae_create(ctypes.byref(self.cfg), _align(self.wbuf.data_ptr()), wb,
+                                      _align(self.ws.data_ptr()), wsb, ctypes.byref(h)))
+        self.h = h
+        self.max_images = max_images
+        self.up = 2 ** (len(vae["ch"]) - 1)
+        n = L.synerdiff_vae_stage_count(self.h)
+        name = ctypes.create_string_buffer(64)
+        self.stages, self.stage_flops = [], []
+        f = ctypes.c_double()
+        for i in range(n):
+            _check(L.synerdiff_vae_stage_name(self.h, i, name, 64))
+            _check(L.synerdiff_vae_stage_flops(self.h, i, ctypes.byref(f)))
+            self.stages.append(name.value.decode())
+            self.stage_flops.append(f.value)
+
+    def load_weights(self, weights):
+        man = vae_manifest(self.cfg)
+        flat = np.concatenate([np.ascontiguousarray(weights[n], np.float32).ravel() for n, _ in man])
+        _check(lib().synerdiff_vae_load_weights(self.h, _ptr(flat), flat.size, self._stream()))
+
+    def _stream(self, stream=None):
+        s = stream if stream is not None else self.torch.cuda.current_stream(self.device)
+        return s.cuda_stream
+
+    def image_shape(self, n):
+        v = self.vae
+        return (n, v["out_c"], v["latent_h"] * self.up, v["latent_w"] * self.up)
+
+    def run(self, latents, begin, end, image=None, stream=None):
+        """Enqueue stages [begin, end) for the batch of latents [n, C, H, W]
+        (fp32 device tensor); returns the image tensor (written when end is
+        the last stage)."""
+        torch = self.torch
+        v = self.vae
+        n = int(latents.shape[0])
+        want = (n, v["latent_c"], v["latent_h"], v["latent_w"])
+        if tuple(latents.shape) != want or latents.dtype != torch.float32 or not latents.is_contiguous() \
+                or latents.device.type != self.device.type:
+            raise ValueError(f"latents: expected a contiguous float32 device tensor of shape {want}")
+        if image is None:
+            image = torch.empty(self.image_shape(n), device=latents.device, dtype=torch.float32)
+        elif tuple(image.shape) != self.image_shape(n) or image.dtype != torch.float32 or not image.is_contiguous():
+            raise ValueError(f"image: expected a contiguous float32 tensor of shape {self.image_shape(n)}")
+        _check(lib().synerdiff_vae_run(self.h, n, _ptr(latents), int(begin), int(end), _ptr(image),
+                                       self._stream(stream)))
+        return image
+
+    def activation(self, i, n):
+        """View of the activation after stage i ([n, H, W, C], channels-last)
+        inside the workspace; valid after a run that ended at stage i + 1."""
+        off = ctypes.c_int64()
+        H, W, C = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        _check(lib().synerdiff_vae_activation(self.h, int(i), ctypes.byref(off), ctypes.byref(H), ctypes.byref(W),
+                                              ctypes.byref(C)))
+        dt = self.torch.bfloat16 if self.vae["dtype"] == "bf16" else self.torch.float32
+        esz = 2 if self.vae["dtype"] == "bf16" else 4
+        base = _align(self.ws.data_ptr()) - self.ws.data_ptr()
+        nbytes = n * H.value * W.value * C.value * esz
+        raw = self.ws[base + off.value: base + off.value + nbytes]
+        return raw.view(dt).reshape(n, H.value, W.value, C.value)
+
+    def decode(self, latents, image=None, stream=None):
+        return self.run(latents, 0, len(self.stages), image=image, stream=stream)
+
+    def close(self):
+        if getattr(self, "h", None):
+            lib().synerdiff_vae_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def plan_sequence(M, N, K, tau, delta, T_lim, exact=False, max_stages=None):
+    """Stage sequence of the inter-concurrency scheduler (Alg. 1, or the exact
+    optimum of Problem P with exact=True).  tau, delta: arrays [B][B][B]
+    (B = bmax + 1) indexed [m][n][k].  Returns (list of (m, n, k), cost, time);
+    raises SynerDiffError when no sequence meets T_lim."""
+    tau = np.ascontiguousarray(tau, np.float64)
+    delta = np.ascontiguousarray(delta, np.float64)
+    B = tau.shape[0]
+    if tau.shape != (B, B, B) or delta.shape != (B, B, B):
+        raise ValueError("tau and delta must be [bmax + 1]^3 arrays")
+    cap = max_stages if max_stages is not None else max(M, 1)
+    seq = np.zeros(3 * cap, np.int32)
+    ns, cost, tm = ctypes.c_int32(), ctypes.c_double(), ctypes.c_double()
+    _check(lib().synerdiff_plan_sequence(int(M), int(N), int(K), B - 1, _ptr(tau), _ptr(delta), float(T_lim),
+                                         int(bool(exact)), cap, _ptr(seq), ctypes.byref(ns), ctypes.byref(cost),
+                                         ctypes.byref(tm)))
+    return [tuple(int(x) for x in seq[3 * t:3 * t + 3]) for t in range(ns.value)], cost.value, tm.value

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(CSRC, "_build")
 LIB = os.path.join(HERE, "libsynerdiff.so")
-SOURCES = ["manifest.cpp", "unet.cpp", "ops.cpp", "gemm.hip", "attention.hip", "misc.hip", "output.hip"]
+SOURCES = ["manifest.cpp", "unet.cpp", "ops.cpp", "gemm.hip", "attention.hip", "misc.hip", "output.hip", "vae.cpp", "vae_kernels.hip", "sched.cpp"]
 
 ARCH = "gfx950"
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-result", "-Wno-unused-variable",
