@@ -24,17 +24,75 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 WORKLOAD = "c3_sd15_mixed32"
+
+
+def unet_flops_per_row(u):
+    """Algorithmic FLOPs of one UNet row: 2 x MACs of every convolution and
+    linear at full size (the upsampling convs as 3x3 convs on the upsampled
+    grid, the context K/V per row), the attention products Q K^T and P V,
+    and the time MLP with every ResBlock's time projection.  803.27 GFLOP for
+    SD-1.5 at 64x64, 6761.24 for the SDXL shape at 128x128."""
+    H, W = u["latent_h"], u["latent_w"]
+    lc, ch, nl = u["latent_c"], u["ch"], len(u["ch"])
+    td, L, D = u["temb_dim"], u["ctx_len"], u["ctx_dim"]
+    f = 2.0 * (u["temb_in"] * td + td * td)
+    if u["add_in"]:
+        f += 2.0 * (u["add_in"] * td + td * td)
+
+    def res(hw, ci, co):
+        return 2.0 * hw * co * 9 * (ci + co) + (2.0 * hw * co * ci if ci != co else 0.0) + 2.0 * td * co
+
+    def tx(n, C, depth):
+        g = 4.0 * n * C * C  # proj_in, proj_out
+        for _ in range(depth):
+            g += 8.0 * n * C * C + 4.0 * n * n * C                       # Q/K/V/O, self-attention
+            g += 4.0 * n * C * C + 4.0 * L * D * C + 4.0 * n * L * C     # Q/O, context K/V, cross-attention
+            g += 24.0 * n * C * C                                        # GEGLU FF (8C up, 4C down)
+        return g
+
+    hw = H * W
+    f += 2.0 * hw * ch[0] * 9 * lc
+    skips, cur = [ch[0]], ch[0]
+    for lv in range(nl):
+        for _ in range(u["n_res"]):
+            f += res(hw, cur, ch[lv])
+            cur = ch[lv]
+            if u["tx_depth"][lv]:
+                f += tx(hw, cur, u["tx_depth"][lv])
+            skips.append(cur)
+        if lv != nl - 1:
+            hw //= 4
+            f += 2.0 * hw * cur * 9 * cur
+            skips.append(cur)
+    f += 2 * res(hw, cur, cur)
+    if u["mid_tx_depth"]:
+        f += tx(hw, cur, u["mid_tx_depth"])
+    for lv in reversed(range(nl)):
+        for _ in range(u["n_res"] + 1):
+            f += res(hw, cur + skips.pop(), ch[lv])
+            cur = ch[lv]
+            if u["tx_depth"][lv]:
+                f += tx(hw, cur, u["tx_depth"][lv])
+        if lv != 0:
+            hw *= 4
+            f += 2.0 * hw * cur * 9 * cur
+    return f + 2.0 * hw * lc * 9 * ch[0]
+
+
 # Other single-GPU workloads bench.py can time with --workload (the default
 # line is the one above): algorithmic FLOPs per UNet row and a description.
 WORKLOADS = {
-    "c3_sd15_mixed32": (803.27e9, "SD-1.5-shaped UNet, latent 4x64x64, bf16; 32 requests at seeded timesteps, "
+    "c3_sd15_mixed32": (None, "SD-1.5-shaped UNet, latent 4x64x64, bf16; 32 requests at seeded timesteps, "
                                   "16 under Skip-CFG -> 48 packed rows; guidance U[5,9]; 77x768 contexts; "
                                   "UNet + CFG combine + DDIM per step"),
-    "c2_sd15_cfg8": (803.27e9, "SD-1.5-shaped UNet, latent 4x64x64, bf16; 8 requests, all with CFG -> 16 rows; "
+    "c2_sd15_cfg8": (None, "SD-1.5-shaped UNet, latent 4x64x64, bf16; 8 requests, all with CFG -> 16 rows; "
                                "guidance 7.5; 77x768 contexts; UNet + CFG combine + DDIM per step"),
-    "c4_sdxl_cfg8": (6761.24e9, "SDXL-shaped UNet, latent 4x128x128, bf16, channels 320/640/1280, "
+    "c4_sdxl_cfg8": (None, "SDXL-shaped UNet, latent 4x128x128, bf16, channels 320/640/1280, "
                                 "transformer depths 0/2/10, 64-wide heads; 8 requests, all with CFG -> 16 rows; "
                                 "77x2048 contexts, pooled 1280 + 6 time ids; UNet + CFG combine + DDIM per step"),
+    "c6_sd21_v": (None, "SD-2.1-shaped UNet, latent 4x96x96 (768 px), bf16, 64-wide heads, 77x1024 contexts, "
+                        "v-prediction; 8 requests, all with CFG -> 16 rows; guidance 7.5; UNet + CFG combine + "
+                        "DDIM per step"),
 }
 METRIC = "UNet rows·steps/sec + % bf16 MFMA peak, SD-1.5-shape, 32-req mixed-CFG batch"
 PEAK_BF16 = 2.5166e15  # dense bf16 MFMA, 256 CU x 4096 FLOP/clk x 2.4 GHz
@@ -233,9 +291,10 @@ def main():
     from paper_2605_08835_amd import UNet
 
     wl = args.workload
-    flop_per_row, description = WORKLOADS[wl]
+    _, description = WORKLOADS[wl]
     spec = get_config(wl)
     unet = spec["unet"]
+    flop_per_row = unet_flops_per_row(unet)
     t0 = time.time()
     weights = make_weights(wl)
     req = make_requests(wl)

@@ -34,6 +34,11 @@ SDXL = dict(
     schedule="scaled_linear", n_steps=50,
 )
 
+# SD-2.1 (768 px): the SD-1.5 layout with 64-wide heads (5/10/20/20 heads),
+# linear proj_in/proj_out (the per-pixel linear both shapes use here), a
+# 1024-wide text context and v-prediction; 96x96 latents.
+SD21 = dict(SD15, latent_h=96, latent_w=96, heads=0, head_dim=64, ctx_dim=1024, prediction="v")
+
 TINY = dict(
     latent_c=4, latent_h=16, latent_w=16, ch=(32, 64), n_res=1,
     tx_depth=(1, 1), mid_tx_depth=1, heads=4, head_dim=0, gn_groups=8,
@@ -83,6 +88,13 @@ CONFIGS = {
                                  mid_tx_depth=2),
                       requests=2, t=("uniform",), cfg=("fixed", (1, 0)),
                       guidance=("uniform", 5.0, 9.0)),
+    # SD-2.1 shape (v-prediction, 64-wide heads, 1024-wide context): 8 requests
+    # with CFG at 768 px, and the same layers at 16x16 for parity.
+    "c6_sd21_v": dict(unet=SD21, requests=8, t=("uniform",), cfg=("all",), guidance=("fixed_all", 7.5)),
+    "t_sd21_16": dict(unet=_with(SD21, latent_h=16, latent_w=16), requests=3, t=("uniform",),
+                      cfg=("fixed", (1, 0, 1)), guidance=("uniform", 5.0, 9.0)),
+    "t_tiny_f32_v": dict(unet=_with(TINY, prediction="v", schedule="scaled_linear"), requests=2,
+                         t=("uniform",), cfg=("fixed", (1, 0)), guidance=("uniform", 5.0, 9.0)),
     "t_tiny_f32_ragged": dict(unet=_with(TINY, latent_h=12, latent_w=20),
                               requests=3, t=("uniform",), cfg=("fixed", (0, 1, 1)),
                               guidance=("uniform", 5.0, 9.0)),

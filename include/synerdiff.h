@@ -99,6 +99,17 @@ size_t synerdiff_workspace_bytes(const sd_unet_config* cfg);
 sd_status synerdiff_unet_create(const sd_unet_config* cfg, void* d_weights, size_t weights_bytes,
                                 void* d_workspace, size_t workspace_bytes, sd_unet** out);
 
+/* A handle for another latent size that uses the packed weights of `src`
+ * (no second copy, no load): for serving requests of several resolutions
+ * (the paper's requests are 512, 768 or 1024 px, Sec. IV-A) with one set of
+ * weights, one handle per resolution, each step over one resolution's
+ * ragged batch.  cfg must equal src's config in every field except
+ * latent_h, latent_w and max_requests.  The weights buffer stays owned by
+ * src's caller and must outlive this handle; loading weights through either
+ * handle updates both. */
+sd_status synerdiff_unet_create_shared(const sd_unet_config* cfg, const sd_unet* src, void* d_workspace,
+                                       size_t workspace_bytes, sd_unet** out);
+
 /* Load all parameters: h_params holds every manifest tensor, fp32, row-major,
  * concatenated in manifest order (n_floats = sum of their sizes).  The
  * library repacks them (bf16 for SD_BF16) into d_weights.  Synchronous: the
@@ -146,6 +157,16 @@ sd_status synerdiff_alphas_cumprod(int32_t schedule, double out[1000]);
 /* DDIM (eta = 0) coefficients of x' = A x + B eps for t -> t_prev, with
  * abar_prev = 1 when t_prev < 0.  Host only. */
 sd_status synerdiff_ddim_coef(const double* alphas_cumprod, int32_t t, int32_t t_prev, float out_AB[2]);
+
+/* The same update for a v-prediction UNet (SD-2.x; Salimans & Ho 2022):
+ * the network predicts v = sqrt(abar) eps - sqrt(1 - abar) x0, the guidance
+ * combine acts on v, and x' = A x + B v with
+ *   A = sqrt(abar_prev abar_t) + sqrt((1 - abar_prev)(1 - abar_t)),
+ *   B = sqrt((1 - abar_prev) abar_t) - sqrt(abar_prev (1 - abar_t)),
+ * which is the DDIM step through x0 = sqrt(abar_t) x - sqrt(1 - abar_t) v and
+ * eps = sqrt(1 - abar_t) x + sqrt(abar_t) v.  Pass these (A, B) to
+ * synerdiff_unet_step; d_eps_out then holds the guided v.  Host only. */
+sd_status synerdiff_ddim_coef_v(const double* alphas_cumprod, int32_t t, int32_t t_prev, float out_AB[2]);
 
 /* Per-kernel timing of the step (the offline-profiling measurements of
  * Sec. III-C: latency of the UNet step's components).  While enabled, the

@@ -37,6 +37,18 @@ def ddim_step(x, eps, a_t, a_prev):
     return math.sqrt(a_prev) * x0 + math.sqrt(1.0 - a_prev) * eps
 
 
+def ddim_step_v(x, v, a_t, a_prev):
+    """DDIM update (eta = 0) for a v-prediction model (Salimans & Ho 2022,
+    as SD-2.x is trained): the network predicts v = sqrt(a_t) eps -
+    sqrt(1 - a_t) x0, so x0 = sqrt(a_t) x - sqrt(1 - a_t) v and
+    eps = sqrt(1 - a_t) x + sqrt(a_t) v; then
+    x' = sqrt(a_prev) x0 + sqrt(1 - a_prev) eps."""
+    x = np.asarray(x, F)
+    x0 = math.sqrt(a_t) * x - math.sqrt(1.0 - a_t) * v
+    eps = math.sqrt(1.0 - a_t) * x + math.sqrt(a_t) * v
+    return math.sqrt(a_prev) * x0 + math.sqrt(1.0 - a_prev) * eps
+
+
 def ddim_coefficients(a_t, a_prev):
     """(A, B) with DDIM's x' = A x + B eps, from expanding ddim_step."""
     A = math.sqrt(a_prev / a_t)
@@ -53,6 +65,10 @@ def unet_step_request(cfg, W, x, t, t_prev, cfg_on, w, ctx, ctx_null, abar,
                       pooled=None, pooled_null=None, time_ids=None, want_eps=False, parts=None):
     """One request's step: returns x' (and the guided eps when asked).
 
+    For a v-prediction UNet (cfg["prediction"] == "v") the network's output
+    is v; guidance combines the two branches' v the same way, and the update
+    is ddim_step_v.
+
     With CFG on both the conditional and the unconditional UNet evaluations
     run and are combined; with Skip-CFG only the conditional one runs and its
     output is used as is (the unconditional branch is bypassed, Sec. III-B).
@@ -67,7 +83,8 @@ def unet_step_request(cfg, W, x, t, t_prev, cfg_on, w, ctx, ctx_null, abar,
         eps = eps_c
     if parts is not None:
         parts["eps_c"], parts["eps_u"] = eps_c, eps_u
-    xn = ddim_step(x, eps, abar_at(abar, t), abar_at(abar, t_prev))
+    step = ddim_step_v if cfg.get("prediction", "eps") == "v" else ddim_step
+    xn = step(x, eps, abar_at(abar, t), abar_at(abar, t_prev))
     return (xn, eps) if want_eps else xn
 
 

@@ -9,3 +9,4 @@ that needs it does, and raises if it is missing.
 from .binding import (UNet, UNetConfig, alphas_cumprod, config_from_dict, ddim_coef,  # noqa: F401
                       lib, manifest, row_plan, SynerDiffError, VAE, VAEConfig, vae_config_from_dict, vae_manifest,
                       vae_chunk_plan, chunk_cost, plan_sequence)
+from .multires import MultiResolutionUNet  # noqa: F401,E402

@@ -69,6 +69,9 @@ _SIG = {
     "synerdiff_alphas_cumprod": (ctypes.c_int, [ctypes.c_int32, _P]),
     "synerdiff_ddim_coef": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _P]),
     "synerdiff_unet_destroy": (None, [_P]),
+    "synerdiff_ddim_coef_v": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32, _P]),
+    "synerdiff_unet_create_shared": (ctypes.c_int, [ctypes.POINTER(UNetConfig), _P, _P, ctypes.c_size_t,
+                                                    ctypes.POINTER(_P)]),
     "synerdiff_profile": (ctypes.c_int, [_P, ctypes.c_int32]),
     "synerdiff_profile_read": (ctypes.c_int, [_P, ctypes.POINTER(KernelStat), ctypes.c_int32,
                                               ctypes.POINTER(ctypes.c_int32), ctypes.c_int32]),
@@ -207,17 +210,21 @@ def alphas_cumprod(schedule):
     return out
 
 
-def ddim_coef(abar, t, t_prev):
+def ddim_coef(abar, t, t_prev, prediction="eps"):
+    """(A, B) of x' = A x + B out for an eps- or v-prediction UNet."""
     abar = np.ascontiguousarray(abar, np.float64)
     out = np.zeros(2, np.float32)
-    _check(lib().synerdiff_ddim_coef(_ptr(abar), int(t), int(t_prev), _ptr(out)))
+    f = lib().synerdiff_ddim_coef_v if prediction == "v" else lib().synerdiff_ddim_coef
+    _check(f(_ptr(abar), int(t), int(t_prev), _ptr(out)))
     return float(out[0]), float(out[1])
 
 
 class UNet:
     """One UNet handle over torch-allocated device buffers."""
 
-    def __init__(self, unet, max_requests, device=None):
+    def __init__(self, unet, max_requests, device=None, share_weights_with=None):
+        """share_weights_with: another UNet of the same architecture (any
+        latent size); this handle then uses its packed weights."""
         import torch
         self.torch = torch
         self.unet = unet
@@ -228,11 +235,18 @@ class UNet:
         self.act_dtype = torch.bfloat16 if unet["dtype"] == "bf16" else torch.float32
         wb = L.synerdiff_weights_bytes(ctypes.byref(self.cfg))
         wsb = L.synerdiff_workspace_bytes(ctypes.byref(self.cfg))
-        self.wbuf = torch.empty(wb + 256, dtype=torch.uint8, device=self.device)
         self.ws = torch.empty(wsb + 256, dtype=torch.uint8, device=self.device)
-        wp, sp = _align(self.wbuf.data_ptr()), _align(self.ws.data_ptr())
+        sp = _align(self.ws.data_ptr())
         h = ctypes.c_void_p()
-        _check(L.synerdiff_unet_create(ctypes.byref(self.cfg), wp, wb, sp, wsb, ctypes.byref(h)))
+        if share_weights_with is not None:
+            self.wbuf = share_weights_with.wbuf  # keeps the shared buffer alive
+            self._shared_from = share_weights_with
+            _check(L.synerdiff_unet_create_shared(ctypes.byref(self.cfg), share_weights_with.h, sp, wsb,
+                                                  ctypes.byref(h)))
+        else:
+            self.wbuf = torch.empty(wb + 256, dtype=torch.uint8, device=self.device)
+            wp = _align(self.wbuf.data_ptr())
+            _check(L.synerdiff_unet_create(ctypes.byref(self.cfg), wp, wb, sp, wsb, ctypes.byref(h)))
         self.h = h
         self.weights_bytes, self.workspace_bytes = wb, wsb
         self.schedule_abar = {}
@@ -251,7 +265,8 @@ class UNet:
         if schedule not in self.schedule_abar:
             self.schedule_abar[schedule] = alphas_cumprod(schedule)
         ab = self.schedule_abar[schedule]
-        return np.array([ddim_coef(ab, t, tp) for t, tp in zip(timesteps, t_prev)], np.float32)
+        pred = self.unet.get("prediction", "eps")
+        return np.array([ddim_coef(ab, t, tp, pred) for t, tp in zip(timesteps, t_prev)], np.float32)
 
     def step(self, latents, timesteps, cfg_on, guidance, ctx_cond, ctx_uncond, coef, out=None,
              eps_out=None, pooled_cond=None, pooled_uncond=None, time_ids=None, stream=None):

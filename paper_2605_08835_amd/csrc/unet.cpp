@@ -1302,6 +1302,48 @@ sd_status synerdiff_ddim_coef(const double* ac, int32_t t, int32_t t_prev, float
   return SD_OK;
 }
 
+sd_status synerdiff_ddim_coef_v(const double* ac, int32_t t, int32_t t_prev, float out_AB[2]) {
+  if (!ac || !out_AB) return fail(SD_ERR_INVALID_ARG, "NULL argument");
+  if (t < 0 || t > 999 || t_prev > 999 || t_prev >= t) return fail(SD_ERR_INVALID_ARG, "need 0 <= t_prev < t <= 999 or t_prev < 0");
+  // x0 = sqrt(a) x - sqrt(1 - a) v, eps = sqrt(1 - a) x + sqrt(a) v,
+  // x' = sqrt(ap) x0 + sqrt(1 - ap) eps
+  const double a = ac[t], ap = t_prev < 0 ? 1.0 : ac[t_prev];
+  out_AB[0] = (float)(sqrt(ap * a) + sqrt((1.0 - ap) * (1.0 - a)));
+  out_AB[1] = (float)(sqrt((1.0 - ap) * a) - sqrt(ap * (1.0 - a)));
+  return SD_OK;
+}
+
+sd_status synerdiff_unet_create_shared(const sd_unet_config* cfg, const sd_unet* src, void* d_workspace,
+                                       size_t workspace_bytes, sd_unet** out) {
+  std::string why;
+  if (!out) return fail(SD_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (!cfg || !src) return fail(SD_ERR_INVALID_ARG, "NULL argument");
+  if (!get_config(cfg, why)) return fail(SD_ERR_UNSUPPORTED, why);
+  sd_unet_config a = *cfg, b = src->cfg;
+  a.latent_h = b.latent_h;
+  a.latent_w = b.latent_w;
+  a.max_requests = b.max_requests;
+  if (memcmp(&a, &b, sizeof(a)) != 0)
+    return fail(SD_ERR_INVALID_ARG, "configs may differ only in latent_h, latent_w and max_requests");
+  if (!d_workspace || ((uintptr_t)d_workspace & 255))
+    return fail(SD_ERR_INVALID_ARG, "workspace must be non-NULL and 256-byte aligned");
+  sd_unet* h = skeleton(cfg);
+  if (h->wtotal != src->wtotal) {
+    delete h;
+    return fail(SD_ERR_UNSUPPORTED, "internal: weight layouts differ");
+  }
+  if (workspace_bytes < h->wsbytes) {
+    delete h;
+    return fail(SD_ERR_WORKSPACE, "workspace buffer too small");
+  }
+  h->wdev = src->wdev;
+  h->wbytes = src->wbytes;
+  h->ws = (uint8_t*)d_workspace;
+  *out = h;
+  return SD_OK;
+}
+
 sd_status synerdiff_unet_step(sd_unet* h, int32_t n_req, const float* lat_in, const int32_t* ts,
                               const uint8_t* cfg_on, const float* guidance, const void* ctx_c,
                               const void* ctx_u, const float* pool_c, const float* pool_u,

@@ -6,7 +6,7 @@ import pytest
 
 import oracle
 from fixtures import get_config, make_requests
-from tests.gpu_util import gpu_step, log, rel_l2
+from tests.gpu_util import gpu_step, log, rel_l2, to_dev
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -175,3 +175,56 @@ def test_ten_chained_steps(weights_cache):
         errs = [rel_l2(g["latents"][r], o["latents"][r]) for r in range(3)]
         log(f"  chained step {step}: rel L2 {['%.2e' % e for e in errs]}")
     assert max(errs) <= 5e-2
+
+
+def test_v_prediction_tiny_f32_step(weights_cache):
+    """v-prediction (SD-2.x): the same kernels with the v-form (A, B)."""
+    check("t_tiny_f32_v", weights_cache)
+
+
+def test_sd21_shape_16px_step(weights_cache):
+    """SD-2.1 layout (64-wide heads, 1024-wide context, v-prediction) at 16x16."""
+    check("t_sd21_16", weights_cache)
+
+
+def test_c6_sd21_768px_sampled(weights_cache):
+    """SD-2.1 at 768 px (96x96 latents), 8 requests with CFG: request 2
+    recomputed by the oracle."""
+    check("c6_sd21_v", weights_cache, only=[2])
+
+
+def test_mixed_resolutions_share_weights(weights_cache):
+    """Requests at 16x16 and 24x24 latents in one step through handles that
+    share one weight copy: each request matches the oracle, and the 16x16
+    group is bit-identical to a standalone handle."""
+    from paper_2605_08835_amd import MultiResolutionUNet
+    wl = "t_sd15_16"
+    unet = get_config(wl)["unet"]
+    W = weights_cache(wl)
+    mr = MultiResolutionUNet(unet, {(16, 16): 3, (24, 24): 2})
+    mr.load_weights(W)
+    base = make_requests(wl)
+    rng = np.random.default_rng(3)
+    big = dict(base, latents=rng.standard_normal((2, 4, 24, 24)).astype(np.float32),
+               timesteps=np.array([640, 90]), t_prev=np.array([620, 70]), cfg_on=np.array([1, 0], np.uint8),
+               guidance=np.array([6.5, 6.5], np.float32), ctx_cond=base["ctx_cond"][:2])
+    act = mr.act_dtype
+    unc = to_dev(base["ctx_uncond"], act)
+    groups = {}
+    for size, r in (((16, 16), base), ((24, 24), big)):
+        groups[size] = dict(latents=to_dev(r["latents"], torch.float32), timesteps=r["timesteps"], cfg_on=r["cfg_on"],
+                            guidance=r["guidance"], ctx_cond=to_dev(r["ctx_cond"], act),
+                            coef=mr.coefficients(r["schedule"], r["timesteps"], r["t_prev"]))
+    outs = mr.step(groups, unc)
+    torch.cuda.synchronize()
+    for size, r in (((16, 16), base), ((24, 24), big)):
+        cfg = dict(unet, latent_h=size[0], latent_w=size[1])
+        ref = oracle.unet_step(cfg, W, r)
+        got = outs[size].cpu().double().numpy()
+        for i in range(len(r["timesteps"])):
+            err = rel_l2(got[i], ref[i])
+            log(f"  mixed resolution {size} request {i}: rel L2 {err:.3e}")
+            assert err <= TOL_LAT["bf16"], (size, i, err)
+    alone, _ = gpu_step(model_for(wl, weights_cache), base, eps=False)
+    assert np.array_equal(outs[(16, 16)].cpu().double().numpy(), alone)
+    mr.close()

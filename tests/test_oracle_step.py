@@ -6,7 +6,7 @@ import pytest
 
 import oracle
 from fixtures import get_config, make_requests, make_weights, manifest, param_count
-from fixtures.configs import SD15, SDXL, TINY
+from fixtures.configs import SD21, SD15, SDXL, TINY
 from oracle import sampler
 from oracle.unet import Weights, unet_eps
 
@@ -45,6 +45,21 @@ def test_ddim_forward_consistency(a_t, a_prev):
     assert np.allclose(A * x + B * eps, xn, atol=1e-10)
 
 
+@pytest.mark.parametrize("a_t,a_prev", [(0.05, 0.07), (0.3, 0.9), (0.999, 1.0), (4e-5, 6e-5)])
+def test_ddim_v_forward_consistency(a_t, a_prev):
+    """v-prediction: with x noised from x0 and eps at a_t and the model
+    predicting v = sqrt(a_t) eps - sqrt(1 - a_t) x0 exactly, the update lands
+    on x0 noised with the same eps at a_prev (and a_prev = a_t is the
+    identity, a_prev = 1 returns x0)."""
+    x0, eps = rng.standard_normal((4, 5, 5)), rng.standard_normal((4, 5, 5))
+    x = math.sqrt(a_t) * x0 + math.sqrt(1 - a_t) * eps
+    v = math.sqrt(a_t) * eps - math.sqrt(1 - a_t) * x0
+    assert np.allclose(sampler.ddim_step_v(x, v, a_t, a_prev), math.sqrt(a_prev) * x0 + math.sqrt(1 - a_prev) * eps,
+                       atol=1e-10)
+    assert np.allclose(sampler.ddim_step_v(x, v, a_t, a_t), x, atol=1e-12)
+    assert np.allclose(sampler.ddim_step_v(x, v, a_t, 1.0), x0, atol=1e-10)
+
+
 def test_ddim_identity_and_final_step():
     x, eps = rng.standard_normal(10), rng.standard_normal(10)
     assert np.allclose(sampler.ddim_step(x, eps, 0.4, 0.4), x, atol=1e-14)
@@ -70,6 +85,8 @@ def test_public_parameter_counts():
     assert param_count(SD15) == 859_520_964
     assert param_count(SDXL) == 2_567_463_684
     assert param_count(TINY) == 1_055_044
+    # SD-2.x: 1024-wide text context, 64-wide heads (no parameters) and linear projections (same count)
+    assert param_count(SD21) == 865_910_724
 
 
 @pytest.fixture(scope="module")
