@@ -90,6 +90,20 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, bf16* lds, int o
 #endif
 }
 
+// Workgroup barrier for the direct-to-LDS pipelines.  __syncthreads()
+// carries a workgroup release fence, for which the compiler waits for every
+// outstanding load that writes LDS (vmcnt(0)), including the prefetches of
+// later K stages, so each stage would have only one compute phase to land.
+// The kernels instead wait with an explicit vmcnt for the loads of the stage
+// they are about to read, then meet here: every wave's loads of that stage
+// have landed once all waves have passed.  The empty asm statements keep
+// the compiler from moving LDS accesses across the barrier.
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 template <int WAITN>
 __device__ __forceinline__ void wait_vmcnt() {
   // s_waitcnt with only the vector-memory counter limited to WAITN

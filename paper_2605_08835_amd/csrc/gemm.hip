@@ -262,16 +262,33 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 
   const int lr = lane & 31, hq = 4 * (lane >> 5);
   const int cpr = OW / 8;  // 16-byte chunks per row
   const bf16* resid = reinterpret_cast<const bf16*>(e.resid);
+  // Residual rows (never with GEGLU, so a row has WC / 8 chunks): every load
+  // of a 32-row group is issued before the first is used, and the next
+  // group's loads are in flight while this group is finished, so the
+  // epilogue waits for memory about once instead of once per chunk.
+  constexpr int RCH = WC / 8, RPL = 32 * RCH / 64;
+  static_assert((32 * RCH) % 64 == 0, "residual chunks spread evenly over the lanes");
+  bf16x8 rres[RPL];
+  auto load_resid = [&](int mrow0) {
+#pragma unroll
+    for (int u = 0; u < RPL; ++u) {
+      const int c = lane + 64 * u, row = c / RCH, ch = c - row * RCH;
+      const int m = mrow0 + row;
+      bf16x8 r = {};
+      if (m < a.M) r = *reinterpret_cast<const bf16x8*>(resid + (long)m * e.ldr + ncol0 + ch * 8);
+      rres[u] = r;
+    }
+  };
+  if (resid) load_resid(m0 + wm * (BM / WM));
   static_for<0, TM>([&](auto I) {
     const int mrow0 = m0 + wm * (BM / WM) + I.value * 32;
     if (resid) {  // (not with GEGLU)
-      for (int c = lane; c < 32 * cpr; c += 64) {
-        const int row = c / cpr, ch = c - row * cpr;
-        const int m = mrow0 + row;
-        bf16x8 r = {};
-        if (m < a.M) r = *reinterpret_cast<const bf16x8*>(resid + (long)m * e.ldr + ncol0 + ch * 8);
-        *reinterpret_cast<bf16x8*>(R + row * LD + ch * 8) = r;
+#pragma unroll
+      for (int u = 0; u < RPL; ++u) {
+        const int c = lane + 64 * u, row = c / RCH, ch = c - row * RCH;
+        *reinterpret_cast<bf16x8*>(R + row * LD + ch * 8) = rres[u];
       }
+      if (I.value + 1 < TM) load_resid(mrow0 + 32);
       asm volatile("" ::: "memory");  // (one wave's LDS accesses complete in order)
     }
     static_for<0, TN>([&](auto J) {
@@ -802,8 +819,7 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
       wait_vmcnt<LPT_MIN>();
     else
       wait_vmcnt<0>();
-    asm volatile("" ::: "memory");  // the LDS was written behind the compiler's back
-    __syncthreads();
+    stage_barrier();
     if (kt + DNS - 1 < nk) issue(kb + kt + DNS - 1, (kt + DNS - 1) % DNS);
     const bf16* Ab = As + (kt % DNS) * BM * DK;
     const bf16* Bb = Bs + (kt % DNS) * BN * DK;

@@ -71,6 +71,12 @@ CONV_CASES = [
     # more blocks than fit on the chip at once (ragged, split K)
     (130, 32, 32, 64, 0, 160, 3, 1, 0, False),
     (150, 8, 8, 640, 0, 320, 3, 1, 0, False),
+    # row-halo kernel (stride-1 3x3 beyond 8x8): split K whose second half starts
+    # inside a channel block's kernel row (19 blocks, 171 K tiles), concat sources
+    (2, 16, 16, 608, 0, 160, 3, 1, 0, False),
+    (3, 16, 16, 320, 320, 320, 3, 1, 0, False),
+    (2, 24, 40, 96, 64, 160, 3, 1, 0, False),
+    (1, 17, 9, 32, 0, 160, 3, 1, 0, False),
 ]
 
 
