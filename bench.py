@@ -171,13 +171,31 @@ def stored_traffic():
     return float(mb.group(1))
 
 
-def summarize(stats_dir=None, fetch_dir=None, write_dir=None, copy_bytes=None):
+def _per_dispatch(d, counters):
+    """{dispatch id: (kernel name, {counter: value})} from a --pmc run's CSV."""
+    import csv
+    import glob
+    f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+    out = {}
+    for r in csv.DictReader(open(f)):
+        if r["Counter_Name"] in counters:
+            name, vals = out.setdefault(r["Dispatch_Id"], (r["Kernel_Name"], {}))
+            vals[r["Counter_Name"]] = vals.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return out
+
+
+def summarize(stats_dir=None, fetch_dir=None, write_dir=None, copy_bytes=None, sq_dir=None):
     """Markdown summary of rocprofv3 output: per-kernel statistics (from a
-    --kernel-trace --stats run) and, from two --pmc runs, the HBM bytes per
-    GEMM launch calibrated on the plain copy kernel of copy_bytes each way."""
+    --kernel-trace --stats run); from two --pmc runs, the HBM bytes per
+    GEMM launch calibrated on the plain copy kernel of copy_bytes each way,
+    and with the statistics run as well, every kernel class's bytes per
+    launch and bandwidth; from a --pmc run of MfmaUtil, VALUBusy,
+    GRBM_GUI_ACTIVE (and LDS counters), each class's MFMA and VALU busy
+    fractions weighted by the dispatches' active cycles."""
     import csv
     import glob
     out = []
+    class_us = {}
     if stats_dir:
         f = glob.glob(os.path.join(stats_dir, "**", "*kernel_stats.csv"), recursive=True)[0]
         rows = list(csv.DictReader(open(f)))
@@ -197,6 +215,7 @@ def summarize(stats_dir=None, fetch_dir=None, write_dir=None, copy_bytes=None):
         out.append("|---|---|---|---|")
         for cls, (calls, ns) in sorted(tot.items(), key=lambda kv: -kv[1][1]):
             out.append(f"| {cls} | {calls} | {ns / 1e6:.3f} | {ns / max(calls, 1) / 1e3:.1f} |")
+            class_us[cls] = ns / max(calls, 1) / 1e3
     if fetch_dir and write_dir:
         def per_dispatch(d, counter):
             f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
@@ -227,6 +246,48 @@ def summarize(stats_dir=None, fetch_dir=None, write_dir=None, copy_bytes=None):
         out.append(f"| GEMM write bytes (scaled) | {g_w * 1024 * kw:.4e} |")
         out.append(f"| traffic_bytes_per_launch | {per:.4e} |")
         out.append(f"| gemm.hip sha256 | {source_digest(GEMM_SOURCE)} |")
+        if class_us:
+            # every class: scaled bytes per launch (a split-K reduction and a
+            # GroupNorm finalize are charged to their launch, as in the timings)
+            byc = {}
+            for lst, k in ((fetch, kf), (write, kw)):
+                for n, v in lst:
+                    cls = kernel_class(n)
+                    if cls:
+                        b = byc.setdefault(cls, [0.0, 0])
+                        b[0] += v * 1024 * k
+            for n, _ in fetch:
+                cls = kernel_class(n)
+                if cls and "splitk_reduce" not in n and "gn_finalize" not in n:
+                    byc[cls][1] += 1
+            out.append("")
+            out.append("| class | launches | HBM bytes per launch (fetch + write) | avg us per launch | GB/s |")
+            out.append("|---|---|---|---|---|")
+            for cls, (b, nl) in sorted(byc.items(), key=lambda kv: -kv[1][0]):
+                if nl and cls in class_us:
+                    per_l = b / nl
+                    out.append(f"| {cls} | {nl} | {per_l:.4e} | {class_us[cls]:.1f} | "
+                               f"{per_l / (class_us[cls] * 1e-6) / 1e9:.0f} |")
+    if sq_dir:
+        names = ("MfmaUtil", "VALUBusy", "GRBM_GUI_ACTIVE", "SQ_LDS_BANK_CONFLICT", "SQ_INSTS_LDS")
+        acc = {}
+        for _, (n, v) in _per_dispatch(sq_dir, names).items():
+            cls = kernel_class(n)
+            if not cls or "GRBM_GUI_ACTIVE" not in v:
+                continue
+            a = acc.setdefault(cls, [0.0, 0.0, 0.0, 0.0, 0.0, 0])
+            g = v["GRBM_GUI_ACTIVE"]
+            a[0] += g
+            a[1] += v.get("MfmaUtil", 0.0) * g
+            a[2] += v.get("VALUBusy", 0.0) * g
+            a[3] += v.get("SQ_LDS_BANK_CONFLICT", 0.0)
+            a[4] += v.get("SQ_INSTS_LDS", 0.0)
+            a[5] += 1
+        out.append("")
+        out.append("| class | dispatches | MfmaUtil % | VALUBusy % | LDS bank-conflict cycles per LDS instruction |")
+        out.append("|---|---|---|---|---|")
+        for cls, a in sorted(acc.items(), key=lambda kv: -kv[1][0]):
+            out.append(f"| {cls} | {a[5]} | {a[1] / a[0]:.1f} | {a[2] / a[0]:.1f} | {a[3] / max(a[4], 1):.3f} |")
     return "\n".join(out)
 
 
@@ -273,12 +334,12 @@ def main():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="run a plain copy kernel of MIB MiB each way first (counter calibration)")
     ap.add_argument("--summarize", nargs="*", metavar="DIR",
-                    help="print a markdown summary of rocprofv3 output: STATS_DIR [FETCH_DIR WRITE_DIR] "
+                    help="print a markdown summary of rocprofv3 output: STATS_DIR [FETCH_DIR WRITE_DIR [SQ_DIR]] "
                          "(the copy size comes from --calibrate-copy)")
     args = ap.parse_args()
     if args.summarize is not None:
-        d = args.summarize + [None] * 3
-        print(summarize(d[0], d[1], d[2], args.calibrate_copy * 2**20))
+        d = [x or None for x in args.summarize] + [None] * 4
+        print(summarize(d[0], d[1], d[2], args.calibrate_copy * 2**20, d[3]))
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the step shards by request with no collective, "
