@@ -75,6 +75,12 @@ CONFIGS = {
     "c5_sd15_serve": dict(unet=SD15, requests=32, iterations=1000,
                           arrival_rate=4.0, steps_range=(20, 50),
                           skip_after=0.6, guidance=("uniform", 5.0, 9.0)),
+    # A small serving loop for tests: a narrow bf16 UNet on 16x16 latents
+    # (the 16x16 VAE test decoder's input), 2-4 steps per request, cap 4.
+    "t_serve_tiny": dict(unet=_with(TINY, dtype="bf16", ch=(64, 128), heads=2, gn_groups=32, ctx_len=11,
+                                    ctx_dim=64, schedule="scaled_linear"),
+                         requests=4, iterations=30, arrival_rate=1.5, steps_range=(2, 4), skip_after=0.6,
+                         guidance=("uniform", 5.0, 9.0)),
     # Smaller parity workloads with the same kernels' shapes and tails.
     "t_tiny_bf16": dict(unet=_with(TINY, dtype="bf16", ch=(64, 128), heads=2,
                                    gn_groups=32, ctx_len=11, ctx_dim=64,

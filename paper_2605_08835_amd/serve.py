@@ -10,9 +10,17 @@ occupy a contiguous prefix, so a retiring request is replaced by the last
 active one (two device-to-device copies).  All denoising work is the C-ABI
 step; this module only keeps per-request bookkeeping on the host.
 
-    python -m paper_2605_08835_amd.serve --iterations 1000
-prints one JSON line with rows*steps/s and the per-step device-time
-p50 / p99 of the SD-1.5-shaped serving workload.
+With VAE Chunking (Sec. III-B) finished latents queue for decoding; a
+decode job of up to `vae_batch` images runs in c chunks on a second stream,
+one chunk beside each UNet step, and both streams join at the end of every
+iteration (one concurrent round).  The load-adaptive feedback controller
+(Sec. III-D) sets the Skip-CFG threshold and c from the queue length.
+
+    python -m paper_2605_08835_amd.serve --iterations 1000 [--vae vae_sd15
+        --chunks C --controller --c-max CMAX]
+prints one JSON line with rows*steps/s (device time and wall clock), the
+per-iteration device-time p50 / p99, request latencies in iterations and,
+with a VAE, images decoded per second.
 """
 import argparse
 import json
@@ -24,7 +32,8 @@ from collections import deque
 
 import numpy as np
 
-from .binding import UNet, alphas_cumprod, ddim_coef
+from .binding import VAE, UNet, alphas_cumprod, ddim_coef, vae_chunk_plan
+from .control import FeedbackController
 
 
 class ContinuousBatcher:
@@ -112,10 +121,100 @@ class ContinuousBatcher:
         return done
 
 
-def run(workload="c5_sd15_serve", iterations=1000, weights=None, log=None, snapshot_at=()):
+def _stage_ms(vae, z, stream, reps=3):
+    """Solo milliseconds of every decoder stage for the batch z (median of reps)."""
+    import torch
+    ns = len(vae.stages)
+    acc = np.zeros((reps, ns))
+    img = torch.empty(vae.image_shape(z.shape[0]), device=z.device)
+    for r in range(reps + 1):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(ns)]
+        for i in range(ns):
+            evs[i][0].record(stream)
+            vae.run(z, i, i + 1, image=img, stream=stream)
+            evs[i][1].record(stream)
+        torch.cuda.synchronize()
+        if r:  # the first pass warms up
+            acc[r - 1] = [a.elapsed_time(b) for a, b in evs]
+    return np.median(acc, axis=0)
+
+
+class VaeChunker:
+    """VAE Chunking in the serving loop (Sec. III-B): finished latents queue
+    for decoding; a decode job of up to `batch` images runs in c chunks of
+    about equal solo time, one chunk per iteration on its own stream,
+    concurrently with that iteration's UNet step."""
+
+    def __init__(self, vae, batch, stream, keep=False):
+        import torch
+        self.torch = torch
+        self.v = vae
+        self.batch = batch
+        self.stream = stream
+        self.keep = keep
+        self.kept = []           # with keep: (ids, latents, images) of every finished job
+        self.z = None
+        self.img = None
+        self.pending = deque()  # (request id, latent [C, H, W] device tensor)
+        self.job = None          # dict(ids, n, bounds, next)
+        self.stage_cost = None
+        self.plans = {}
+        self.done = []           # (request id, iteration the decode finished)
+
+    def setup(self, latent_shape, device):
+        torch = self.torch
+        self.z = torch.zeros((self.batch,) + tuple(latent_shape), device=device)
+        self.img = torch.empty(self.v.image_shape(self.batch), device=device)
+        self.stage_cost = _stage_ms(self.v, self.z[:1], self.stream)
+
+    def bounds(self, c):
+        c = max(1, min(c, len(self.v.stages)))
+        if c not in self.plans:
+            self.plans[c] = vae_chunk_plan(self.stage_cost, c)
+        return self.plans[c]
+
+    def start_job(self, c, stream):
+        """Take up to `batch` pending latents (copied on `stream`, the UNet's,
+        after the step that finished them) as the next decode job."""
+        if self.job is not None or not self.pending:
+            return
+        ids = []
+        while self.pending and len(ids) < self.batch:
+            rid, lat = self.pending.popleft()
+            with self.torch.cuda.stream(stream):
+                self.z[len(ids)].copy_(lat)
+            ids.append(rid)
+        self.job = dict(ids=ids, n=len(ids), bounds=self.bounds(c), next=0)
+
+    def run_chunk(self, it):
+        """Enqueue the job's next chunk on the VAE stream; returns True if one ran."""
+        j = self.job
+        if j is None:
+            return False
+        b, e = j["bounds"][j["next"]], j["bounds"][j["next"] + 1]
+        self.v.run(self.z[:j["n"]], b, e, image=self.img[:j["n"]], stream=self.stream)
+        j["next"] += 1
+        if j["next"] == len(j["bounds"]) - 1:
+            self.done += [(rid, it) for rid in j["ids"]]
+            if self.keep:
+                with self.torch.cuda.stream(self.stream):
+                    self.kept.append((j["ids"], self.z[:j["n"]].clone(), self.img[:j["n"]].clone()))
+            self.job = None
+        return True
+
+
+def run(workload="c5_sd15_serve", iterations=1000, weights=None, log=None, snapshot_at=(), vae=None,
+        vae_batch=4, chunks=1, controller=None, keep_images=False):
     """Serve the workload's arrival trace for `iterations` iterations.
     Returns a result dict (and the snapshots requested by iteration index:
-    the step inputs, the latents before and after the step)."""
+    the step inputs, the latents before and after the step).
+
+    vae: a VAE-decoder configuration name (fixtures.vae) to decode finished
+    requests with VAE Chunking on a second stream, `chunks` chunks per decode
+    job of up to `vae_batch` images; controller: a FeedbackController that
+    sets the Skip-CFG threshold and the chunk count from the queue length
+    every iteration (Sec. III-D); keep_images: return every decode job's
+    latents and images under snaps["images"]."""
     import torch
 
     from fixtures import (get_config, make_weights, serve_arrivals, serve_null_context,
@@ -134,48 +233,117 @@ def run(workload="c5_sd15_serve", iterations=1000, weights=None, log=None, snaps
     arrivals = serve_arrivals(workload, iterations)
     queue = deque()
     stream = torch.cuda.current_stream(dev)
+    vz = None
+    if vae is not None:
+        from fixtures.vae import VAE_CONFIGS, make_vae_weights
+        vcfg = dict(VAE_CONFIGS[vae]["vae"])
+        vh = VAE(vcfg, max_images=vae_batch, device=dev)
+        vh.load_weights(make_vae_weights(vae))
+        vz = VaeChunker(vh, vae_batch, torch.cuda.Stream(device=dev), keep=keep_images)  # default priority
+        vz.setup((unet["latent_c"], unet["latent_h"], unet["latent_w"]), dev)
+    if controller is not None:
+        b.skip_after = controller.skip_after
+        chunks = controller.c
     ev = []
     rows_total, req_steps, finished = 0, 0, 0
     host_ms = []
     snaps = {}
+    arrived_at = {}
+    finished_at = {}
+    vae_rounds = 0
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
     for it in range(iterations):
         for rid, S, w in arrivals[it]:
             queue.append((rid, S, w))
+            arrived_at[rid] = it
+        if controller is not None:
+            b.skip_after, chunks = controller.update(len(queue))
         while queue and b.n < cap:
             rid, S, w = queue.popleft()
             lat, ctx = serve_request_inputs(workload, rid)
             b.admit(rid, torch.from_numpy(lat).to(dev), torch.from_numpy(ctx).to(dev).to(act), S, w)
-        if b.n == 0:
+        if b.n == 0 and (vz is None or vz.job is None):
             continue
         before = b.lat[:b.n].clone() if it in snapshot_at else None
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         h0 = time.perf_counter()
+        if vz is not None:
+            # one concurrent round: both streams start after both finished
+            # the previous round (and the VAE stream after the latent copies)
+            stream.wait_stream(vz.stream)
+            vz.stream.wait_stream(stream)
         e0.record(stream)
-        inp = b.step(stream=stream)
+        inp = None
+        if b.n:
+            inp = b.step(stream=stream)
+        if vz is not None:
+            vae_rounds += int(vz.run_chunk(it))
+            stream.wait_stream(vz.stream)
         e1.record(stream)
         host_ms.append(1e3 * (time.perf_counter() - h0))
         ev.append((e0, e1))
-        rows_total += int(inp["n"] + inp["cfg_on"].sum())
-        req_steps += inp["n"]
-        if before is not None:
-            snaps[it] = dict(inputs=inp, before=before.cpu().numpy(), after=b.lat[:b.n].cpu().numpy(),
-                             ctx=b.ctx[:b.n].float().cpu().numpy())
-        finished += len(b.retire())
+        if inp is not None:
+            rows_total += int(inp["n"] + inp["cfg_on"].sum())
+            req_steps += inp["n"]
+            if before is not None:
+                snaps[it] = dict(inputs=inp, before=before.cpu().numpy(), after=b.lat[:b.n].cpu().numpy(),
+                                 ctx=b.ctx[:b.n].float().cpu().numpy())
+        done = b.retire()
+        finished += len(done)
+        for rid, lat in done:
+            finished_at[rid] = it
+            if vz is not None:
+                vz.pending.append((rid, lat))
+        if vz is not None:
+            vz.start_job(chunks, stream)
         if log and it % 100 == 0:
-            log(f"iteration {it}: active {b.n}, queued {len(queue)}, finished {finished}")
+            extra = f", decode queue {len(vz.pending)}" if vz is not None else ""
+            ctl = f", skip_after {b.skip_after:.2f}, c {chunks}" if controller is not None else ""
+            log(f"iteration {it}: active {b.n}, queued {len(queue)}, finished {finished}{extra}{ctl}")
     torch.cuda.synchronize()
+    wall_s = time.perf_counter() - wall0
     dev_ms = np.array([a.elapsed_time(c) for a, c in ev])
     m.close()
+    lo, hi = spec["steps_range"]
+    desc = (f"{workload}: {unet['dtype']} UNet, {unet['latent_h']}x{unet['latent_w']} latents, widths {unet['ch']}; "
+            f"Poisson({spec['arrival_rate']:g}) arrivals per iteration, {lo}-{hi} steps per request, batch cap {cap}, "
+            f"Skip-CFG after {100 * spec['skip_after']:.0f}% of a request's steps")
+    if vz is not None:
+        desc += f"; VAE decoder {vae} on a second stream, jobs of up to {vae_batch} images"
+    if controller is not None:
+        desc += "; feedback controller on the queue length"
     res = {
-        "workload": "SD-1.5-shaped UNet, 64x64 latents, bf16; Poisson(4) arrivals per iteration, "
-                    "20-50 steps per request, batch cap 32, Skip-CFG after 60% of a request's steps",
+        "workload": desc,
         "iterations": iterations, "steps_run": len(dev_ms), "finished": finished, "queued_at_end": len(queue),
         "rows_steps_per_s": rows_total / (dev_ms.sum() / 1e3),
         "request_steps_per_s": req_steps / (dev_ms.sum() / 1e3),
+        "rows_steps_per_s_wall": rows_total / wall_s, "wall_s": wall_s,
         "mean_rows": rows_total / max(len(dev_ms), 1),
         "step_ms_p50": float(np.percentile(dev_ms, 50)), "step_ms_p99": float(np.percentile(dev_ms, 99)),
         "host_ms_p50": float(np.percentile(host_ms, 50)), "host_ms_p99": float(np.percentile(host_ms, 99)),
     }
+    lat_it = [finished_at[r] - arrived_at[r] + 1 for r in finished_at]
+    if lat_it:
+        res["denoise_latency_iterations_p50"] = float(np.percentile(lat_it, 50))
+        res["denoise_latency_iterations_p99"] = float(np.percentile(lat_it, 99))
+    if vz is not None:
+        img_it = [it - arrived_at[r] + 1 for r, it in vz.done]
+        res.update(images_decoded=len(vz.done), vae_chunk_rounds=vae_rounds,
+                   images_per_s=len(vz.done) / (dev_ms.sum() / 1e3),
+                   decode_queue_at_end=len(vz.pending) + (vz.job["n"] if vz.job else 0),
+                   chunk_bounds={str(c): bb for c, bb in vz.plans.items()},
+                   stage_ms=[round(float(x), 4) for x in vz.stage_cost])
+        if img_it:
+            res["image_latency_iterations_p50"] = float(np.percentile(img_it, 50))
+            res["image_latency_iterations_p99"] = float(np.percentile(img_it, 99))
+        if keep_images:
+            torch.cuda.synchronize()
+            snaps["images"] = [(ids, z.cpu().numpy(), im.cpu().numpy()) for ids, z, im in vz.kept]
+        vz.v.close()
+    if controller is not None:
+        res["controller"] = dict(final_skip_after=controller.skip_after, final_c=controller.c,
+                                 changes=controller.log[:50], n_changes=len(controller.log))
     return res, snaps
 
 
@@ -183,11 +351,18 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--iterations", type=int, default=1000)
     ap.add_argument("--workload", default="c5_sd15_serve")
+    ap.add_argument("--vae", default="", help="decode finished requests with this VAE (e.g. vae_sd15)")
+    ap.add_argument("--vae-batch", type=int, default=4)
+    ap.add_argument("--chunks", type=int, default=1, help="VAE Chunking granularity c")
+    ap.add_argument("--controller", action="store_true", help="load-adaptive feedback controller")
+    ap.add_argument("--c-max", type=int, default=4)
     args = ap.parse_args()
     root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
     if root not in sys.path:
         sys.path.insert(0, root)
-    res, _ = run(args.workload, args.iterations, log=lambda s: print(s, file=sys.stderr, flush=True))
+    ctl = FeedbackController(c0=args.chunks, c_max=max(args.c_max, args.chunks)) if args.controller else None
+    res, _ = run(args.workload, args.iterations, log=lambda s: print(s, file=sys.stderr, flush=True),
+                 vae=args.vae or None, vae_batch=args.vae_batch, chunks=args.chunks, controller=ctl)
     print(json.dumps(res), flush=True)
 
 

@@ -34,3 +34,29 @@ def test_serving_loop_and_oracle_replay(weights_cache):
         err = rel_l2(snap["after"][i], ref)
         log(f"  replay request {inp['ids'][i]} t={inp['t'][i]} cfg={inp['cfg_on'][i]}: rel L2 {err:.3e}")
         assert err <= 2e-2
+
+
+def test_serving_loop_with_vae_chunking_and_controller():
+    """The loop with finished requests decoded in chunks on a second stream
+    beside the UNet steps, and the feedback controller moving the Skip-CFG
+    threshold and c: every decoded image is bit-identical to a plain decode
+    of the same latents on one stream."""
+    from fixtures.vae import VAE_CONFIGS, make_vae_weights
+    from paper_2605_08835_amd import VAE, serve
+    from paper_2605_08835_amd.control import FeedbackController
+    ctl = FeedbackController(c0=2, c_max=3, window=2, grow=0.1, shrink=0.1)
+    res, snaps = serve.run("t_serve_tiny", iterations=30, log=log, vae="vae_t16", vae_batch=2, chunks=2,
+                           controller=ctl, keep_images=True)
+    log(f"serving loop with VAE: {res}")
+    assert res["finished"] > 0 and res["images_decoded"] > 0 and res["vae_chunk_rounds"] >= 2
+    assert 0.3 - 1e-9 <= res["controller"]["final_skip_after"] <= 0.6 + 1e-9
+    assert 2 <= res["controller"]["final_c"] <= 3
+    jobs = snaps["images"]
+    assert sum(len(ids) for ids, _, _ in jobs) == res["images_decoded"]
+    v = VAE(VAE_CONFIGS["vae_t16"]["vae"], max_images=2)
+    v.load_weights(make_vae_weights("vae_t16"))
+    for ids, z, img in jobs:
+        ref = v.decode(torch.from_numpy(z).cuda())
+        torch.cuda.synchronize()
+        assert np.array_equal(ref.cpu().numpy(), img), f"job {ids}"
+    v.close()
