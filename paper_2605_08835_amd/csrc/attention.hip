@@ -273,23 +273,139 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
     }
   };
 
-  fetch(0, rk0, rv0);
-  stage(0, rk0, rv0);
-  if (PF2 && KT < a.Nk) fetch(KT, rk1, rv1);
+  // Heads with the max in the product (d = D16 - 8, a compile-time width):
+  // the padding of K (the ones column d) and of V^T (the ones row d, then
+  // zero rows) is the same for every tile, so it is written into both LDS
+  // buffers once, and a tile moves only its d / 8 data chunks per key and
+  // its d rows of V^T (the general fetch spent more vector instructions on
+  // addressing and masks than the softmax on its maxima).  Keys past the
+  // end load as zeros; the ones row keeps 1 there, which the masked
+  // probabilities (exactly 0) multiply away, so the sums are unchanged.
+  constexpr bool FAST = MF;
+  constexpr int DV = D16 - 8, CK = DV / 8;
+  constexpr int KV = KT * CK, VV = DV * (KT / 8);  // data chunks per tile
+  constexpr int KPF = (KV + NT - 1) / NT, VPF = (VV + NT - 1) / NT;
+  static_assert(!FAST || (KPF <= KPT && VPF <= VPT), "the data chunks fit the fetch registers");
+  auto fetch_data = [&](int k0, bf16x8 (&rk)[KPT], bf16x8 (&rv)[VPT]) {
+#pragma unroll
+    for (int i = 0; i < KPF; ++i) {
+      const int idx = tid + NT * i;
+      if (KV % NT == 0 || idx < KV) {
+        const int key = idx / CK, c = idx - key * CK;
+        bf16x8 v = {};
+        if (k0 + key < a.Nk) v = ld16(K + (long)(k0 + key) * a.k_ld + 8 * c);
+        rk[i] = v;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VPF; ++i) {
+      const int idx = tid + NT * i;
+      if (VV % NT == 0 || idx < VV) {
+        const int dd = idx / (KT / 8), kc = (idx - dd * (KT / 8)) * 8;
+        const int k = k0 + kc;
+        const bf16* src = V + (long)dd * a.v_ld + k;
+        bf16x8 v = {};
+        if (vvec && k + 8 <= a.Nk) {
+          v = ld16(src);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (k + e < a.Nk) v[e] = src[e];
+        }
+        rv[i] = v;
+      }
+    }
+  };
+  auto stage_data = [&](int b, const bf16x8 (&rk)[KPT], const bf16x8 (&rv)[VPT]) {
+#pragma unroll
+    for (int i = 0; i < KPF; ++i) {
+      const int idx = tid + NT * i;
+      if (KV % NT == 0 || idx < KV) {
+        const int key = idx / CK, c = idx - key * CK;
+        *reinterpret_cast<bf16x8*>(&Ks[b][key * LDK + 8 * c]) = rk[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VPF; ++i) {
+      const int idx = tid + NT * i;
+      if (VV % NT == 0 || idx < VV) {
+        const int dd = idx / (KT / 8), kc = (idx - dd * (KT / 8)) * 8;
+        *reinterpret_cast<bf16x8*>(&Vt[b][dd * LDV + kc]) = rv[i];
+      }
+    }
+  };
+  if constexpr (FAST) {
+    // K: chunk DV of every key of both buffers; V^T: rows DV..DP-1 of both
+    for (int c = tid; c < 2 * KT; c += NT) {
+      bf16x8 v = {};
+      v[0] = (bf16)1.0f;
+      *reinterpret_cast<bf16x8*>(&Ks[c / KT][(c % KT) * LDK + DV]) = v;
+    }
+    constexpr int PR = (DP - DV) * (KT / 8);  // padding chunks per buffer
+    for (int c = tid; c < 2 * PR; c += NT) {
+      const int b = c / PR, r = c - b * PR, dd = DV + r / (KT / 8), kc = (r % (KT / 8)) * 8;
+      bf16x8 v = {};
+      if (dd == DV)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = (bf16)1.0f;
+      *reinterpret_cast<bf16x8*>(&Vt[b][dd * LDV + kc]) = v;
+    }
+  }
+  // A tile known to be full, with 16-byte aligned V^T rows: no bounds checks
+  // and no element-wise fallback, so the loop that uses it holds only the
+  // 16-byte loads (a fallback's scalar loads into temporaries make the
+  // compiler wait for every outstanding load before the products).
+  auto fetch_full = [&](int k0, bf16x8 (&rk)[KPT], bf16x8 (&rv)[VPT]) {
+#pragma unroll
+    for (int i = 0; i < KPF; ++i) {
+      const int idx = tid + NT * i;
+      if (KV % NT == 0 || idx < KV) {
+        const int key = idx / CK, c = idx - key * CK;
+        rk[i] = ld16(K + (long)(k0 + key) * a.k_ld + 8 * c);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VPF; ++i) {
+      const int idx = tid + NT * i;
+      if (VV % NT == 0 || idx < VV) {
+        const int dd = idx / (KT / 8), kc = (idx - dd * (KT / 8)) * 8;
+        rv[i] = ld16(V + (long)dd * a.v_ld + k0 + kc);
+      }
+    }
+  };
+  auto fetch_any = [&](int k0, bf16x8 (&rk)[KPT], bf16x8 (&rv)[VPT]) {
+    if constexpr (FAST)
+      fetch_data(k0, rk, rv);
+    else
+      fetch(k0, rk, rv);
+  };
+  auto stage_any = [&](int b, int, const bf16x8 (&rk)[KPT], const bf16x8 (&rv)[VPT]) {
+    if constexpr (FAST)
+      stage_data(b, rk, rv);
+    else
+      stage(b, rk, rv);
+  };
+
+  fetch_any(0, rk0, rv0);
+  stage_any(0, 0, rk0, rv0);
+  if (PF2 && KT < a.Nk) fetch_any(KT, rk1, rv1);
   __syncthreads();
   // One 64-key tile; the last tile, if partial, is a separate instance so
   // the full tiles carry no masking code.
   // fk / fv: the set to fetch the tile after next into; sk / sv: the set
   // holding the next tile, staged at the end.
-  auto tile = [&](auto tl, int k0, int it, bf16x8 (&fk)[KPT], bf16x8 (&fv)[VPT], bf16x8 (&sk)[KPT],
+  // FULL: the tile it fetches is full and V^T is aligned (FAST heads only).
+  auto tile = [&](auto tl, auto ff, int k0, int it, bf16x8 (&fk)[KPT], bf16x8 (&fv)[VPT], bf16x8 (&sk)[KPT],
                   bf16x8 (&sv)[VPT]) {
-    constexpr bool TAIL = decltype(tl)::value;
+    constexpr bool TAIL = decltype(tl)::value, FULL = decltype(ff)::value;
     const int b = it & 1;
     const bool more = k0 + KT < a.Nk;
-    if constexpr (PF2) {
-      if (k0 + 2 * KT < a.Nk) fetch(k0 + 2 * KT, fk, fv);
+    if constexpr (FULL) {
+      fetch_full(k0 + (PF2 ? 2 : 1) * KT, PF2 ? fk : sk, PF2 ? fv : sv);
+    } else if constexpr (PF2) {
+      if (k0 + 2 * KT < a.Nk) fetch_any(k0 + 2 * KT, fk, fv);
     } else {
-      if (more) fetch(k0 + KT, sk, sv);
+      if (more) fetch_any(k0 + KT, sk, sv);
     }
     const bf16* Kb = Ks[b];
     const bf16* Vb = Vt[b];
@@ -335,25 +451,47 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
         for (int g = 0; g < QG; ++g) o[g][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[g], o[g][t], 0, 0, 0);
       }
     }
-    if (more) stage(b ^ 1, sk, sv);
+    if constexpr (FULL && PF2) {
+      // The next tile's data was fetched a tile ago; of the loads issued
+      // since (this tile's fetch), the ones every lane issues are the last
+      // KV / NT + VV / NT in program order, so waiting down to that many
+      // leaves only them in flight.
+      wait_vmcnt<KV / NT + VV / NT>();
+    }
+    if (more) stage_any(b ^ 1, k0 + KT, sk, sv);
     __syncthreads();
   };
   const int nfull = a.Nk / KT;
   int it = 0;
+  // Every load issued so far (the queries, the first tiles) has landed
+  // before the loops start: otherwise the compiler cannot tell, inside the
+  // loop, that the query registers are no longer pending and waits for all
+  // outstanding loads, the prefetch included, before the first product of
+  // every tile.
+  wait_vmcnt<0>();
+  const bool full_ok = FAST && vvec;
   if constexpr (PF2) {
+    // pairs whose fetch targets (tiles it + 2 and it + 3) are both full
+    if (full_ok)
+      for (; (it + 4) * KT <= a.Nk; it += 2) {
+        tile(BC<false>{}, BC<FAST>{}, it * KT, it, rk0, rv0, rk1, rv1);
+        tile(BC<false>{}, BC<FAST>{}, (it + 1) * KT, it + 1, rk1, rv1, rk0, rv0);
+      }
     for (; it + 1 < nfull; it += 2) {
-      tile(BC<false>{}, it * KT, it, rk0, rv0, rk1, rv1);
-      tile(BC<false>{}, (it + 1) * KT, it + 1, rk1, rv1, rk0, rv0);
+      tile(BC<false>{}, BC<false>{}, it * KT, it, rk0, rv0, rk1, rv1);
+      tile(BC<false>{}, BC<false>{}, (it + 1) * KT, it + 1, rk1, rv1, rk0, rv0);
     }
     if (it < nfull) {
-      tile(BC<false>{}, it * KT, it, rk0, rv0, rk1, rv1);
+      tile(BC<false>{}, BC<false>{}, it * KT, it, rk0, rv0, rk1, rv1);
       ++it;
     }
   } else {
-    for (; it < nfull; ++it) tile(BC<false>{}, it * KT, it, rk0, rv0, rk0, rv0);
+    if (full_ok)
+      for (; (it + 2) * KT <= a.Nk; ++it) tile(BC<false>{}, BC<FAST>{}, it * KT, it, rk0, rv0, rk0, rv0);
+    for (; it < nfull; ++it) tile(BC<false>{}, BC<false>{}, it * KT, it, rk0, rv0, rk0, rv0);
   }
   // (the partial last tile fetches and stages nothing)
-  if (nfull * KT < a.Nk) tile(BC<true>{}, nfull * KT, it, rk0, rv0, rk1, rv1);
+  if (nfull * KT < a.Nk) tile(BC<true>{}, BC<false>{}, nfull * KT, it, rk0, rv0, rk1, rv1);
 
   // O^T accumulator: lane holds head dims t*32 + 8(r/4) + 4 lh + [0, 4) of
   // its query; each run of 4 is one 8-byte store.

@@ -179,8 +179,9 @@ class Profiler:
                     for _ in range(reps):
                         if n:
                             r = self.rounds(first, n_unet=m, skip=k, n_vae=n)[0]
-                            self._vae(first[1], ns, n, stream=self.sb)  # finish the decode
-                            self.torch.cuda.synchronize()
+                            if first[1] < ns:  # finish the decode
+                                self._vae(first[1], ns, n, stream=self.sb)
+                                self.torch.cuda.synchronize()
                         else:
                             r = (self._time(lambda: self._unet(m, k, stream=self.sa), self.sa, 1), 0.0)
                         vals.append(r)

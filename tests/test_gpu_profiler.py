@@ -82,6 +82,8 @@ def test_lookup_grid_and_planner(prof):
     from paper_2605_08835_amd.profiler import dense_table
     P, m, v, z, inputs = prof
     R = len(inputs["timesteps"])
+    g1 = P.lookup_grid(1, [1, R], [0, 2], reps=1)  # c = 1: the whole decode in one round
+    assert np.all(np.array(g1["tau"]) > 0)
     g = P.lookup_grid(2, list(range(1, R + 1)), [0, 1, 2], reps=1)
     tau, delta = np.array(g["tau"]), np.array(g["delta"])
     assert tau.shape == (R, 3, 3) and np.all(tau > 0)
