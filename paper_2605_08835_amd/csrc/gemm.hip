@@ -260,12 +260,11 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 
   const int OW = geglu ? WC / 2 : WC;  // output columns of the wave
   const int ncol0 = (geglu ? n0 / 2 : n0) + wn * OW;
   const int lr = lane & 31, hq = 4 * (lane >> 5);
-  const int cpr = OW / 8;  // 16-byte chunks per row
   const bf16* resid = reinterpret_cast<const bf16*>(e.resid);
   // Residual rows (never with GEGLU, so a row has WC / 8 chunks): every load
   // of a 32-row group is issued before the first is used, and the next
-  // group's loads are in flight while this group is finished, so the
-  // epilogue waits for memory about once instead of once per chunk.
+  // group's loads are in flight while this group is stored, so the epilogue
+  // waits for memory about once instead of once per chunk.
   constexpr int RCH = WC / 8, RPL = 32 * RCH / 64;
   static_assert((32 * RCH) % 64 == 0, "residual chunks spread evenly over the lanes");
   bf16x8 rres[RPL];
@@ -280,6 +279,15 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 
     }
   };
   if (resid) load_resid(m0 + wm * (BM / WM));
+  // The bias of the columns the lane finishes in 32-column tile J (columns
+  // nt + 8 q + hq + [0, 4); with GEGLU q = 0, 1 are the value and q = 2, 3
+  // the gate columns), loaded one tile ahead of its use.
+  auto load_bias = [&](int J, float4 (&b)[4]) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      b[q] = e.bias ? *reinterpret_cast<const float4*>(e.bias + n0 + wn * WC + J * 32 + 8 * q + hq)
+                    : make_float4(0.f, 0.f, 0.f, 0.f);
+  };
   static_for<0, TM>([&](auto I) {
     const int mrow0 = m0 + wm * (BM / WM) + I.value * 32;
     if (resid) {  // (not with GEGLU)
@@ -288,10 +296,11 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 
         const int c = lane + 64 * u, row = c / RCH, ch = c - row * RCH;
         *reinterpret_cast<bf16x8*>(R + row * LD + ch * 8) = rres[u];
       }
-      if (I.value + 1 < TM) load_resid(mrow0 + 32);
       asm volatile("" ::: "memory");  // (one wave's LDS accesses complete in order)
     }
     static_for<0, TN>([&](auto J) {
+      float4 bj[4];
+      load_bias(J.value, bj);
       const f32x16 v = acc[I.value][J.value];
       const int nt = n0 + wn * WC + J.value * 32;
       const int m = mrow0 + lr;
@@ -300,12 +309,13 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 
         // packed columns 32t + u (a) and 32t + 16 + u (gate) -> channel 16t + u
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
-          const int n = nt + 8 * q + hq;
+          const float ba[4] = {bj[q].x, bj[q].y, bj[q].z, bj[q].w};
+          const float bg[4] = {bj[q + 2].x, bj[q + 2].y, bj[q + 2].z, bj[q + 2].w};
           float x[4];
 #pragma unroll
           for (int k = 0; k < 4; ++k) {
-            const float av = fmaf(v[4 * q + k], rs, e.bias[n + k]);
-            const float g = fmaf(v[4 * (q + 2) + k], rs, e.bias[n + 16 + k]);
+            const float av = fmaf(v[4 * q + k], rs, ba[k]);
+            const float g = fmaf(v[4 * (q + 2) + k], rs, bg[k]);
             x[k] = av * gelu_as(g);
           }
           bf16x4 o;
@@ -317,11 +327,10 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int n = nt + 8 * q + hq;
-          float x[4] = {v[4 * q] * rs, v[4 * q + 1] * rs, v[4 * q + 2] * rs, v[4 * q + 3] * rs};
-          if (e.bias) {
-            const float4 b = *reinterpret_cast<const float4*>(e.bias + n);
-            x[0] += b.x; x[1] += b.y; x[2] += b.z; x[3] += b.w;
-          }
+          // (one rounding for scale and bias, written out so that it does not
+          // depend on the compiler's contraction choices; bj is 0 without a bias)
+          float x[4] = {fmaf(v[4 * q], rs, bj[q].x), fmaf(v[4 * q + 1], rs, bj[q].y),
+                        fmaf(v[4 * q + 2], rs, bj[q].z), fmaf(v[4 * q + 3], rs, bj[q].w)};
           if (e.tbias && m < a.M) {
             const float4 b = *reinterpret_cast<const float4*>(e.tbias + (long)(m / e.hw) * e.tb_ld + e.tb_off + n);
             x[0] += b.x; x[1] += b.y; x[2] += b.z; x[3] += b.w;
@@ -344,13 +353,40 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 
       }
     });
     asm volatile("" ::: "memory");
-    for (int c = lane; c < 32 * cpr; c += 64) {
-      const int row = c / cpr, ch = c - row * cpr;
-      const int m = mrow0 + row;
-      if (m < a.M && ncol0 + ch * 8 < (geglu ? a.N / 2 : a.N))
-        *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(e.out) + out_row(e, m) * e.ldo + ncol0 + ch * 8) =
-            *reinterpret_cast<const bf16x8*>(R + row * LD + ch * 8);
-    }
+    if (resid && I.value + 1 < TM) load_resid(mrow0 + 32);
+    // Every LDS read of a run of chunks is issued before its first store,
+    // so the stores wait for the LDS once per run rather than once per
+    // chunk; the row width in chunks is a compile-time constant per case.
+    auto store_rows = [&](auto cpc) {
+      constexpr int CP = decltype(cpc)::value, NCH = 32 * CP / 64, SH = (NCH + 1) / 2;
+      static_assert((32 * CP) % 64 == 0, "row chunks spread evenly over the lanes");
+      const int nout = geglu ? a.N / 2 : a.N;
+#pragma unroll
+      for (int h = 0; h < NCH; h += SH) {
+        bf16x8 ob[SH];
+#pragma unroll
+        for (int u = 0; u < SH; ++u) {
+          if (h + u < NCH) {
+            const int c = lane + 64 * (h + u), row = c / CP, ch = c - row * CP;
+            ob[u] = *reinterpret_cast<const bf16x8*>(R + row * LD + ch * 8);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < SH; ++u) {
+          if (h + u < NCH) {
+            const int c = lane + 64 * (h + u), row = c / CP, ch = c - row * CP;
+            const int m = mrow0 + row;
+            if (m < a.M && ncol0 + ch * 8 < nout)
+              *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(e.out) + out_row(e, m) * e.ldo + ncol0 + ch * 8) =
+                  ob[u];
+          }
+        }
+      }
+    };
+    if (geglu)
+      store_rows(IC<WC / 16>{});
+    else
+      store_rows(IC<WC / 8>{});
     asm volatile("" ::: "memory");
   });
 }
