@@ -1126,6 +1126,10 @@ hipError_t launch_gemm(DType dt, const GemmArgs& args, hipStream_t s) {
       } else {
         launch_bf16<128, 160, 64, 4, 1>(a, s);
       }
+    } else if (a.N % 128 == 0 && a.ksplit == 1 && launch_dma<256, 128, 4, 1, 3, 2>(a, s)) {
+      // widths that are multiples of 128 but not of 160 (the VAE decoder's
+      // 128 / 256 / 512): the same direct-to-LDS pipeline in 256x128 tiles,
+      // waves of 64x128, three K stages (2 x 73.7 KB of LDS)
     } else if (a.N % 128 == 0 || a.N > 64) {
       if (nblk(256, 128) >= want)
         launch_bf16<256, 128, 64, 2, 2>(a, s);

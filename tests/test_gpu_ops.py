@@ -62,7 +62,7 @@ CONV_CASES = [
     (2, 4, 4, 640, 640, 320, 3, 1, 0, False),
     (3, 4, 4, 1280, 0, 160, 3, 2, 0, False),
     (2, 2, 2, 640, 0, 320, 3, 1, 1, False),
-    # enough rows for the 256x320 eight-wave tiles (ragged, concat, stride 2, upsampling)
+    # many rows (ragged, concat, stride 2, upsampling)
     (65, 32, 32, 64, 0, 320, 3, 1, 0, False),
     (32, 32, 32, 64, 64, 640, 3, 1, 0, False),
     (64, 64, 64, 32, 0, 320, 3, 2, 0, False),
@@ -71,12 +71,19 @@ CONV_CASES = [
     # more blocks than fit on the chip at once (ragged, split K)
     (130, 32, 32, 64, 0, 160, 3, 1, 0, False),
     (150, 8, 8, 640, 0, 320, 3, 1, 0, False),
-    # row-halo kernel (stride-1 3x3 beyond 8x8): split K whose second half starts
-    # inside a channel block's kernel row (19 blocks, 171 K tiles), concat sources
+    # stride-1 3x3 beyond 8x8: split K whose second half starts inside a
+    # channel block's kernel row (19 blocks, 171 K tiles), concat sources
     (2, 16, 16, 608, 0, 160, 3, 1, 0, False),
     (3, 16, 16, 320, 320, 320, 3, 1, 0, False),
     (2, 24, 40, 96, 64, 160, 3, 1, 0, False),
     (1, 17, 9, 32, 0, 160, 3, 1, 0, False),
+    # widths that are multiples of 128 but not of 160 (the VAE decoder's): the
+    # 256x128 direct-to-LDS tiles (ragged, concat, upsampling, 1x1, many rows)
+    (2, 12, 12, 128, 0, 128, 3, 1, 0, False),
+    (3, 9, 10, 256, 0, 256, 3, 1, 0, False),
+    (2, 6, 6, 512, 0, 256, 3, 1, 1, False),
+    (2, 16, 16, 128, 128, 256, 1, 1, 0, False),
+    (40, 16, 16, 128, 0, 512, 3, 1, 0, False),
 ]
 
 
