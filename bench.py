@@ -394,14 +394,17 @@ def main():
         step()
     torch.cuda.synchronize()
     log(f"warmup done ({args.warmup} steps)")
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # one event between consecutive steps: the mean over the whole run is the
+    # metric, the per-step spread (median, min, max) comes from the same events
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    e0.record(stream)
-    for _ in range(args.steps):
+    evs[0].record(stream)
+    for i in range(args.steps):
         step()
-    e1.record(stream)
+        evs[i + 1].record(stream)
     torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
+    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
+    ms = evs[0].elapsed_time(evs[-1]) / args.steps
     log(f"timed {args.steps} steps: {ms:.3f} ms/step")
 
     # Per-kernel-class split: the same steps again with an event after every launch.
@@ -452,6 +455,8 @@ def main():
     res = {
         "metric": METRIC, "value": round(value, 2), "unit": "rows·steps/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 3),
+        "step_ms": {"mean": round(ms, 3), "median": round(float(np.median(per_step)), 3),
+                    "min": round(float(per_step.min()), 3), "max": round(float(per_step.max()), 3)},
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) latents and contexts, random-init N(0,0.02) weights)",
         "config": {"workload": description, "name": wl, "requests": R, "rows": rows,
