@@ -65,10 +65,10 @@ sd_status synerdiff_op_upconv(int32_t dtype, const void* d_x, int32_t n, int32_t
  * (fp32), or, with v_transposed = 1 (required for bf16), at
  * v + j*v_img + c*v_ld + t (channel-major, the layout the step's
  * projections write); O like Q with o_img, o_ld.  Strides in elements.
- * q_log2 = 1 (bf16 only): Q already holds q * scale * log2(e), as the
- * step's projections write it (scale is then unused).  Constraints: d a
- * multiple of 8; bf16: d rounded up to 16 is 16..96, 128, 160, 192 or 256;
- * fp32: d <= 64. */
+ * q_log2 = 1: Q already holds q * scale * log2(e), as the step's bf16
+ * projections write it (scale is then unused).  Constraints: d a multiple
+ * of 8; bf16: d rounded up to 16 is 16..96, 128, 160, 192 or 256; fp32:
+ * d <= 256 (V row-major). */
 sd_status synerdiff_op_attention(int32_t dtype, const void* d_q, int64_t q_ld, int64_t q_img,
                                  const void* d_k, int64_t k_ld, int64_t k_img, const void* d_v,
                                  int64_t v_ld, int64_t v_img, int32_t v_transposed,

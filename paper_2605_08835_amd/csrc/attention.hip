@@ -526,11 +526,10 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
   }
 }
 
-template <int DMAX>
+template <int DMAX, int KTF>
 __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
-  constexpr int KT = 64;
-  __shared__ float Ks[KT * DMAX];
-  __shared__ float Vs[KT * DMAX];
+  __shared__ float Ks[KTF * DMAX];
+  __shared__ float Vs[KTF * DMAX];
   const int tid = threadIdx.x;
   const int img = blockIdx.z, head = blockIdx.y;
   const int q = blockIdx.x * 64 + tid;
@@ -539,6 +538,8 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
   const float* Q = reinterpret_cast<const float*>(a.q) + (long)img * a.q_img + hd;
   const float* K = reinterpret_cast<const float*>(a.k) + (long)kvimg * a.k_img + hd;
   const float* V = reinterpret_cast<const float*>(a.v) + (long)kvimg * a.v_img + hd;
+  // q_log2: Q holds q * scale * log2(e), so a score is a base-2 exponent
+  const bool l2 = a.q_log2 != 0;
   float qv[DMAX], o[DMAX];
 #pragma unroll
   for (int i = 0; i < DMAX; ++i) {
@@ -546,9 +547,9 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
     o[i] = 0.f;
   }
   float m = -INFINITY, l = 0.f;
-  for (int k0 = 0; k0 < a.Nk; k0 += KT) {
+  for (int k0 = 0; k0 < a.Nk; k0 += KTF) {
     __syncthreads();
-    const int nk = min(KT, a.Nk - k0);
+    const int nk = min(KTF, a.Nk - k0);
     for (int idx = tid; idx < nk * d; idx += 64) {
       const int key = idx / d, i = idx - key * d;
       Ks[key * DMAX + i] = K[(long)(k0 + key) * a.k_ld + i];
@@ -560,9 +561,9 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
 #pragma unroll
       for (int i = 0; i < DMAX; ++i)
         if (i < d) sc = fmaf(qv[i], Ks[key * DMAX + i], sc);
-      sc *= a.scale;
+      if (!l2) sc *= a.scale;
       const float mn = fmaxf(m, sc);
-      const float al = expf(m - mn), p = expf(sc - mn);
+      const float al = l2 ? exp2f(m - mn) : expf(m - mn), p = l2 ? exp2f(sc - mn) : expf(sc - mn);
       l = l * al + p;
 #pragma unroll
       for (int i = 0; i < DMAX; ++i)
@@ -632,12 +633,18 @@ hipError_t launch_attention(DType dt, const AttnArgs& a, hipStream_t s) {
       default: return hipErrorInvalidValue;
     }
   } else {
-    if (a.vt || a.q_log2) return hipErrorInvalidValue;
+    if (a.vt || a.d <= 0) return hipErrorInvalidValue;
     dim3 grid((a.Nq + 63) / 64, a.heads, a.imgs);
+    // (the wide heads keep q and o in scratch: the fp32 path is the
+    // reference-precision path for small configurations, not a fast one)
     if (a.d <= 16)
-      attn_f32_kernel<16><<<grid, 64, 0, s>>>(a);
+      attn_f32_kernel<16, 64><<<grid, 64, 0, s>>>(a);
     else if (a.d <= 64)
-      attn_f32_kernel<64><<<grid, 64, 0, s>>>(a);
+      attn_f32_kernel<64, 64><<<grid, 64, 0, s>>>(a);
+    else if (a.d <= 128)
+      attn_f32_kernel<128, 32><<<grid, 64, 0, s>>>(a);
+    else if (a.d <= 256)
+      attn_f32_kernel<256, 16><<<grid, 64, 0, s>>>(a);
     else
       return hipErrorInvalidValue;
   }

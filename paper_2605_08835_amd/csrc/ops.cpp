@@ -122,9 +122,8 @@ sd_status synerdiff_op_attention(int32_t dtype, const void* q, int64_t q_ld, int
   if (bad_dtype(dtype)) return op_fail(SD_ERR_INVALID_ARG, "bad dtype");
   if (!q || !k || !v || !o) return op_fail(SD_ERR_INVALID_ARG, "NULL argument");
   if (n < 0 || heads < 1 || d < 8 || d % 8 || nq < 0 || nk < 1) return op_fail(SD_ERR_INVALID_ARG, "bad shape");
-  if (dtype == SD_BF16 ? !attention_width_ok(d) : d > 64) return op_fail(SD_ERR_UNSUPPORTED, "unsupported head width");
+  if (dtype == SD_BF16 ? !attention_width_ok(d) : d > 256) return op_fail(SD_ERR_UNSUPPORTED, "unsupported head width");
   if ((v_transposed != 0) != (dtype == SD_BF16)) return op_fail(SD_ERR_UNSUPPORTED, "V is transposed for bf16 and only for bf16");
-  if (q_log2 && dtype != SD_BF16) return op_fail(SD_ERR_UNSUPPORTED, "pre-scaled queries are bf16 only");
   if (n == 0 || nq == 0) return SD_OK;
   AttnArgs a;
   memset(&a, 0, sizeof(a));

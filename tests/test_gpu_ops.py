@@ -184,11 +184,9 @@ def test_upconv_rejects_unsupported_widths(ops):
 ])
 def test_attention(ops, dt, qmode, heads, d, nq, nk, scale, cross):
     """bf16 takes V transposed (channel-major, padded token stride, as the
-    step stores it); "log2" passes Q pre-multiplied by scale * log2(e) and
-    rounded once, as the projection epilogue writes it, and the reference
-    uses exactly that Q (divided back in float64)."""
-    if dt == "f32" and (d > 64 or qmode == "log2"):
-        pytest.skip("fp32 attention covers head widths <= 64 with row-major V and plain Q")
+    step stores it), fp32 row-major V; "log2" passes Q pre-multiplied by
+    scale * log2(e) and rounded once, as the projection epilogue writes it,
+    and the reference uses exactly that Q (divided back in float64)."""
     log(f"attention {dt} {qmode} heads={heads} d={d} nq={nq} nk={nk} x{scale} cross={cross}")
     rng = np.random.default_rng(d * 1000 + nq)
     C = heads * d
