@@ -102,6 +102,26 @@ class ContinuousBatcher:
         self.k[:n] += 1
         return inputs
 
+    def permute(self, order):
+        """Reorder the active prefix: slot i takes the request in slot order[i]."""
+        n = self.n
+        idx = self.torch.as_tensor(np.asarray(order, np.int64), device=self.lat.device)
+        self.lat[:n] = self.lat[:n].index_select(0, idx)
+        self.ctx[:n] = self.ctx[:n].index_select(0, idx)
+        o = np.asarray(order)
+        self.ids[:n] = [self.ids[i] for i in order]
+        self.k[:n], self.S[:n], self.w[:n] = self.k[:n][o], self.S[:n][o], self.w[:n][o]
+
+    def step_range(self, lo, hi, cfg, stream=None):
+        """One UNet step for the requests in slots [lo, hi) with the given
+        CFG flags (a request past its threshold may still run with CFG)."""
+        t, tp, _ = self.plan()
+        t, tp = t[lo:hi], tp[lo:hi]
+        coef = self.coefficients(t, tp)
+        self.m.step(self.lat[lo:hi], t, np.asarray(cfg, np.uint8), self.w[lo:hi], self.ctx[lo:hi], self.null_ctx,
+                    coef, out=self.lat[lo:hi], stream=stream)
+        self.k[lo:hi] += 1
+
     def retire(self):
         """Remove finished requests; returns their ids and final latents."""
         done = []
@@ -347,6 +367,155 @@ def run(workload="c5_sd15_serve", iterations=1000, weights=None, log=None, snaps
     return res, snaps
 
 
+def assign_stages(seq, cfg):
+    """Slot order and CFG flags for a stage sequence [(m, n, k)] (Problem P,
+    Sec. III-D) over the requests of one window: stage t takes k_t requests
+    past their Skip-CFG threshold (cfg 0), which run without CFG, then
+    m_t - k_t others with CFG (requests still under their threshold first;
+    past-threshold ones fill in when those run out).  Returns (order, flags,
+    stage bounds)."""
+    elig = [i for i in range(len(cfg)) if cfg[i] == 0]
+    rest = [i for i in range(len(cfg)) if cfg[i] != 0]
+    order, flags, bounds = [], [], [0]
+    for m, _, k in seq:
+        take = [elig.pop(0) for _ in range(k)]
+        flags += [0] * k
+        for _ in range(m - k):
+            take.append(rest.pop(0) if rest else elig.pop(0))
+            flags.append(1)
+        order += take
+        bounds.append(len(order))
+    if elig or rest or len(order) != len(cfg):
+        raise ValueError("stage sequence does not cover the window's requests")
+    return order, flags, bounds
+
+
+def run_planned(workload="c5_sd15_serve", iterations=300, lut=None, policy="exact", vae="vae_sd15", nmax=4,
+                alpha=0.1, saturate=True, log=None):
+    """The serving loop driven by the inter-concurrency scheduler (Sec.
+    III-D): every window gives each active request one step; the M steps, the
+    N finished images waiting for decoding (at most nmax) and the K requests
+    past their Skip-CFG threshold are split into concurrent stages (m_t, n_t,
+    k_t) by the planner on the offline lookup table (`lut`: the profiler's
+    lookup grid), each stage one UNet step over m_t requests beside one
+    whole decode of n_t images on a second stream.  policy: "single" (one
+    stage: every step and every decode together), "alg1" (Alg. 1) or
+    "exact" (the optimum of Problem P).  T_lim = (1 + alpha) tau(M, N, K).
+    The objective counts only the decodes' completion times, so where no
+    decode is waiting every stage split ties and the planner returns its
+    first (fewest skips); with saturate, every request past its threshold
+    skips CFG in whichever stage it lands, which only shortens the stages
+    (the latency cap still holds) and keeps the Skip-CFG rule of the other
+    loops."""
+    import torch
+
+    from fixtures import (get_config, make_weights, serve_arrivals, serve_null_context,
+                          serve_request_inputs)
+    from fixtures.vae import VAE_CONFIGS, make_vae_weights
+
+    from .binding import SynerDiffError, plan_sequence
+    from .profiler import dense_table
+    spec = get_config(workload)
+    unet = spec["unet"]
+    cap = spec["requests"]
+    m = UNet(unet, max_requests=cap)
+    m.load_weights(make_weights(workload))
+    dev = torch.device("cuda")
+    act = m.act_dtype
+    b = ContinuousBatcher(m, cap, unet["schedule"], spec["skip_after"])
+    b.set_null_context(torch.from_numpy(serve_null_context(workload)).to(dev).to(act))
+    vh = VAE(dict(VAE_CONFIGS[vae]["vae"]), max_images=nmax, device=dev)
+    vh.load_weights(make_vae_weights(vae))
+    ns = len(vh.stages)
+    z = torch.zeros((nmax, unet["latent_c"], unet["latent_h"], unet["latent_w"]), device=dev)
+    img = torch.empty(vh.image_shape(nmax), device=dev)
+    tau, delta = dense_table(lut, cap)
+    arrivals = serve_arrivals(workload, iterations)
+    queue, pending = deque(), deque()  # pending: (request id, latent, index of the stage that finished it)
+    us, vs = torch.cuda.current_stream(dev), torch.cuda.Stream(device=dev)  # default priorities
+    stages = []  # (start event, end event)
+    finished_at, decoded_at = {}, {}
+    plans, fallbacks, rows_total, req_steps = 0, 0, 0, 0
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    for it in range(iterations):
+        for rid, S, w in arrivals[it]:
+            queue.append((rid, S, w))
+        while queue and b.n < cap:
+            rid, S, w = queue.popleft()
+            lat, ctx = serve_request_inputs(workload, rid)
+            b.admit(rid, torch.from_numpy(lat).to(dev), torch.from_numpy(ctx).to(dev).to(act), S, w)
+        M = b.n
+        N = min(len(pending), nmax, max(M, 1))
+        if M == 0 and N == 0:
+            continue
+        _, _, cfg = b.plan()
+        K = int((cfg == 0).sum())
+        if M == 0:
+            seq = [(0, N, 0)]  # no request to step: a decode-only stage
+        elif policy == "single":
+            seq = [(M, N, K)]
+        else:
+            try:
+                seq, _, _ = plan_sequence(M, N, K, tau, delta, (1 + alpha) * tau[M, N, K], exact=policy == "exact")
+                plans += 1
+            except SynerDiffError:
+                seq = [(M, N, K)]
+                fallbacks += 1
+        order, flags, bounds = assign_stages(seq, cfg) if M else ([], [], [0, 0])
+        if M:
+            b.permute(order)
+            if saturate:
+                flags = [int(cfg[o]) for o in order]
+        for si, (mt, nt, kt) in enumerate(seq):
+            vs.wait_stream(us)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(us)
+            job = []
+            for j in range(nt):
+                rid, lat, _ = pending.popleft()
+                with torch.cuda.stream(us):
+                    z[j].copy_(lat)
+                job.append(rid)
+            if nt:
+                vs.wait_stream(us)
+                vh.run(z[:nt], 0, ns, image=img[:nt], stream=vs)
+            lo, hi = bounds[si], bounds[si + 1]
+            if hi > lo:
+                b.step_range(lo, hi, flags[lo:hi], stream=us)
+            rows_total += (hi - lo) + int(sum(flags[lo:hi]))
+            req_steps += hi - lo
+            us.wait_stream(vs)
+            e1.record(us)
+            stages.append((e0, e1))
+            for rid in job:
+                decoded_at[rid] = len(stages) - 1
+            for i in range(lo, hi):
+                if b.k[i] >= b.S[i]:
+                    finished_at[b.ids[i]] = len(stages) - 1
+        for rid, lat in b.retire():
+            pending.append((rid, lat, finished_at[rid]))
+        if log and it % 50 == 0:
+            log(f"window {it}: active {b.n}, queued {len(queue)}, decode queue {len(pending)}, stages {len(seq)}")
+    torch.cuda.synchronize()
+    wall_s = time.perf_counter() - wall0
+    dur = np.array([a.elapsed_time(c) for a, c in stages])
+    end = np.cumsum(dur)
+    waits = [end[decoded_at[r]] - end[finished_at[r]] for r in decoded_at]
+    m.close()
+    vh.close()
+    res = {
+        "workload": workload, "policy": policy, "windows": iterations, "stages": len(stages),
+        "plans": plans, "fallbacks": fallbacks, "device_ms": float(dur.sum()), "wall_s": wall_s,
+        "rows_steps_per_s": rows_total / dur.sum() * 1e3, "request_steps_per_s": req_steps / dur.sum() * 1e3,
+        "images_decoded": len(decoded_at), "images_per_s": len(decoded_at) / dur.sum() * 1e3,
+        "decode_wait_ms_mean": float(np.mean(waits)) if waits else None,
+        "decode_wait_ms_p50": float(np.percentile(waits, 50)) if waits else None,
+        "decode_wait_ms_p99": float(np.percentile(waits, 99)) if waits else None,
+    }
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--iterations", type=int, default=1000)
@@ -356,10 +525,20 @@ def main():
     ap.add_argument("--chunks", type=int, default=1, help="VAE Chunking granularity c")
     ap.add_argument("--controller", action="store_true", help="load-adaptive feedback controller")
     ap.add_argument("--c-max", type=int, default=4)
+    ap.add_argument("--planner", choices=["single", "alg1", "exact"], default=None,
+                    help="windows planned by the inter-concurrency scheduler on --lut")
+    ap.add_argument("--lut", default="", help="offline profile JSON (paper_2605_08835_amd.profiler --out)")
     args = ap.parse_args()
     root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
     if root not in sys.path:
         sys.path.insert(0, root)
+    if args.planner:
+        with open(args.lut) as f:
+            grid = json.load(f)["lookup_grid"]
+        res = run_planned(args.workload, args.iterations, lut=grid, policy=args.planner, vae=args.vae or "vae_sd15",
+                          nmax=args.vae_batch, log=lambda s: print(s, file=sys.stderr, flush=True))
+        print(json.dumps(res), flush=True)
+        return
     ctl = FeedbackController(c0=args.chunks, c_max=max(args.c_max, args.chunks)) if args.controller else None
     res, _ = run(args.workload, args.iterations, log=lambda s: print(s, file=sys.stderr, flush=True),
                  vae=args.vae or None, vae_batch=args.vae_batch, chunks=args.chunks, controller=ctl)

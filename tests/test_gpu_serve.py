@@ -60,3 +60,22 @@ def test_serving_loop_with_vae_chunking_and_controller():
         torch.cuda.synchronize()
         assert np.array_equal(ref.cpu().numpy(), img), f"job {ids}"
     v.close()
+
+
+def test_planned_windows_decode_every_finished_request():
+    """The loop driven by the stage planner on a synthetic lookup table
+    (latency growing with the requests, the decodes and fewer skips): each
+    policy runs, decodes the finished requests, and the exact planner never
+    leaves a window without a plan."""
+    from paper_2605_08835_amd import serve
+    grid = dict(m_grid=[1, 4], n_grid=[0, 2], k_fracs=[0.0, 1.0],
+                tau=[[[2.0, 1.5], [4.0, 3.5]], [[5.0, 3.0], [7.0, 5.0]]],
+                delta=[[[0.0, 0.0], [3.0, 3.0]], [[0.0, 0.0], [4.0, 4.0]]])
+    for policy in ("single", "alg1", "exact"):
+        res = serve.run_planned("t_serve_tiny", iterations=24, lut=grid, policy=policy, vae="vae_t16", nmax=2,
+                                log=log)
+        log(f"planned serving ({policy}): {res}")
+        assert res["images_decoded"] > 0 and res["stages"] >= 24
+        assert res["decode_wait_ms_mean"] is not None and res["decode_wait_ms_mean"] >= 0
+        if policy == "exact":
+            assert res["fallbacks"] == 0

@@ -43,3 +43,21 @@ def test_schedule_skip_window_and_retirement():
         assert ts[rid][-1] == 0 and ts[rid] == sorted(ts[rid], reverse=True) and len(ts[rid]) == S
     # the final step of a request ends at x0 (abar_prev = 1)
     assert all(np.isfinite(c[2]).all() for c in m.calls)
+
+
+def test_stage_assignment_covers_the_window():
+    """Slots of a planned window (Problem P stages): stage t takes k_t
+    requests past their threshold (run without CFG) and m_t - k_t others,
+    under-threshold ones first."""
+    from paper_2605_08835_amd.serve import assign_stages
+    cfg = [1, 0, 1, 0, 1, 0]
+    order, flags, bounds = assign_stages([(2, 1, 1), (4, 0, 1)], cfg)
+    assert sorted(order) == list(range(6)) and bounds == [0, 2, 6]
+    assert order[:2] == [1, 0] and flags[:2] == [0, 1]          # stage 1: one skip, one with CFG
+    assert flags[2:].count(0) == 1 and cfg[order[2]] == 0        # stage 2: exactly one skip
+    # a skip budget below the eligible count: the others run with CFG
+    order, flags, bounds = assign_stages([(6, 0, 0)], cfg)
+    assert flags == [1] * 6 and order[:3] == [0, 2, 4]
+    import pytest
+    with pytest.raises(ValueError):
+        assign_stages([(3, 0, 0)], cfg)  # does not cover the window
