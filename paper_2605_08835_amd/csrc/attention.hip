@@ -281,8 +281,10 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
   // addressing and masks than the softmax on its maxima).  Keys past the
   // end load as zeros; the ones row keeps 1 there, which the masked
   // probabilities (exactly 0) multiply away, so the sums are unchanged.
-  constexpr bool FAST = MF;
-  constexpr int DV = D16 - 8, CK = DV / 8;
+  // (also the pre-scaled heads whose width is D16 itself with the sum in
+  // the product: no K padding, the V^T ones row at d = D16)
+  constexpr bool FAST = MF || (QS && SF);
+  constexpr int DV = MF ? D16 - 8 : D16, CK = DV / 8;
   constexpr int KV = KT * CK, VV = DV * (KT / 8);  // data chunks per tile
   constexpr int KPF = (KV + NT - 1) / NT, VPF = (VV + NT - 1) / NT;
   static_assert(!FAST || (KPF <= KPT && VPF <= VPT), "the data chunks fit the fetch registers");
@@ -335,12 +337,14 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
     }
   };
   if constexpr (FAST) {
-    // K: chunk DV of every key of both buffers; V^T: rows DV..DP-1 of both
-    for (int c = tid; c < 2 * KT; c += NT) {
-      bf16x8 v = {};
-      v[0] = (bf16)1.0f;
-      *reinterpret_cast<bf16x8*>(&Ks[c / KT][(c % KT) * LDK + DV]) = v;
-    }
+    // K: chunk DV of every key of both buffers (the ones column; none when
+    // DV = D16); V^T: rows DV..DP-1 of both
+    if constexpr (MF)
+      for (int c = tid; c < 2 * KT; c += NT) {
+        bf16x8 v = {};
+        v[0] = (bf16)1.0f;
+        *reinterpret_cast<bf16x8*>(&Ks[c / KT][(c % KT) * LDK + DV]) = v;
+      }
     constexpr int PR = (DP - DV) * (KT / 8);  // padding chunks per buffer
     for (int c = tid; c < 2 * PR; c += NT) {
       const int b = c / PR, r = c - b * PR, dd = DV + r / (KT / 8), kc = (r % (KT / 8)) * 8;
