@@ -281,9 +281,11 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
   // addressing and masks than the softmax on its maxima).  Keys past the
   // end load as zeros; the ones row keeps 1 there, which the masked
   // probabilities (exactly 0) multiply away, so the sums are unchanged.
-  // (also the pre-scaled heads whose width is D16 itself with the sum in
-  // the product: no K padding, the V^T ones row at d = D16)
-  constexpr bool FAST = MF || (QS && SF);
+  // The same holds for every pre-scaled variant, whose width is fixed at
+  // compile time too (d = D16 when the max does not ride in the product):
+  // no K padding then, and the V^T ones row only when the sum rides in PV.
+  // (Not at 128 and above 160, where the extra registers spill.)
+  constexpr bool FAST = QS && (D16 <= 96 || D16 == 160);
   constexpr int DV = MF ? D16 - 8 : D16, CK = DV / 8;
   constexpr int KV = KT * CK, VV = DV * (KT / 8);  // data chunks per tile
   constexpr int KPF = (KV + NT - 1) / NT, VPF = (VV + NT - 1) / NT;
@@ -349,7 +351,7 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
     for (int c = tid; c < 2 * PR; c += NT) {
       const int b = c / PR, r = c - b * PR, dd = DV + r / (KT / 8), kc = (r % (KT / 8)) * 8;
       bf16x8 v = {};
-      if (dd == DV)
+      if (SF && dd == DV)
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = (bf16)1.0f;
       *reinterpret_cast<bf16x8*>(&Vt[b][dd * LDV + kc]) = v;
