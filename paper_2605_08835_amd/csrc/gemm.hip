@@ -391,6 +391,99 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 
   });
 }
 
+// Epilogue of the large wave tiles (128 x 128 per wave, accumulators in
+// AGPRs): each 32-row group of the wave is first written raw (fp32) into a
+// wave-private LDS slab, then finished from there in row-contiguous runs of
+// 8 outputs per lane (bias, time bias, row scale, residual, query scale or
+// GEGLU), with the same arithmetic as the other epilogues.  Reading the
+// accumulators only to copy them keeps the register demand low.
+template <int WC>
+constexpr int SLAB_LD = WC + 4;  // floats per slab row
+
+template <int BM, int BN, int WM, int WN, int TM, int TN>
+__device__ __forceinline__ void epilogue_slab(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int m0, int n0,
+                                              int wm, int wn, int lane, float* R) {
+  constexpr int WC = BN / WN;
+  constexpr int LD = SLAB_LD<WC>;
+  const Epi& e = a.epi;
+  const bool geglu = e.geglu;
+  const int lr = lane & 31, hq = 4 * (lane >> 5);
+  const int nc0 = n0 + wn * WC;                                // first accumulator column of the wave
+  const int ncol0 = geglu ? nc0 / 2 : nc0;                     // first output column
+  const int nout = geglu ? a.N / 2 : a.N;
+  const bf16* resid = reinterpret_cast<const bf16*>(e.resid);  // (never with GEGLU)
+  static_for<0, TM>([&](auto I) {
+    const int mrow0 = m0 + wm * (BM / WM) + I.value * 32;
+    static_for<0, TN>([&](auto J) {
+      const f32x16 v = acc[I.value][J.value];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<float4*>(R + lr * LD + J.value * 32 + 8 * q + hq) =
+            make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+    });
+    asm volatile("" ::: "memory");  // (one wave's LDS accesses complete in order)
+    auto finish = [&](auto cpc) {
+      constexpr int CP = decltype(cpc)::value, NCH = 32 * CP / 64;  // output chunks per row, per lane
+      static_assert((32 * CP) % 64 == 0, "row chunks spread evenly over the lanes");
+      bf16x8 rr[NCH];
+      if (resid) {
+#pragma unroll
+        for (int u = 0; u < NCH; ++u) {
+          const int c = lane + 64 * u, row = c / CP, ch = c - row * CP, m = mrow0 + row;
+          bf16x8 r = {};
+          if (m < a.M) r = *reinterpret_cast<const bf16x8*>(resid + (long)m * e.ldr + ncol0 + ch * 8);
+          rr[u] = r;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < NCH; ++u) {
+        const int c = lane + 64 * u, row = c / CP, ch = c - row * CP, m = mrow0 + row;
+        const float rs = row_scale(e, m, a.M);
+        float x[8];
+        if (geglu) {
+          // output chunk ch: value columns 32 t + 8 h + [0, 8), gate 16 further
+          const int col = (ch >> 1) * 32 + 8 * (ch & 1);
+          const float* src = R + row * LD + col;
+#pragma unroll
+          for (int k = 0; k < 8; ++k) {
+            const float ba = e.bias ? e.bias[nc0 + col + k] : 0.f, bg = e.bias ? e.bias[nc0 + col + 16 + k] : 0.f;
+            const float av = fmaf(src[k], rs, ba);
+            const float g = fmaf(src[16 + k], rs, bg);
+            x[k] = av * gelu_as(g);
+          }
+        } else {
+          const int col = 8 * ch, n = nc0 + col;
+          const float* src = R + row * LD + col;
+#pragma unroll
+          for (int k = 0; k < 8; ++k) x[k] = fmaf(src[k], rs, e.bias ? e.bias[n + k] : 0.f);
+          if (e.tbias && m < a.M) {
+            const float* tb = e.tbias + (long)(m / e.hw) * e.tb_ld + e.tb_off + n;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) x[k] += tb[k];
+          }
+          if (resid) {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) x[k] += (float)rr[u][k];
+          }
+#pragma unroll
+          for (int k = 0; k < 8; ++k)
+            if (n + k < e.qcols) x[k] *= e.qscale;
+        }
+        bf16x8 o;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) o[k] = (bf16)x[k];
+        if (m < a.M && ncol0 + ch * 8 < nout)
+          *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(e.out) + out_row(e, m) * e.ldo + ncol0 + ch * 8) = o;
+      }
+    };
+    if (geglu)
+      finish(IC<WC / 16>{});
+    else
+      finish(IC<WC / 8>{});
+    asm volatile("" ::: "memory");
+  });
+}
+
 // The transposed part of a QKV projection (V written [image][channel][token]
 // for the attention kernel): the wave stages its 32 tokens x WC channels
 // channel-major, then stores 16-byte runs of 8 consecutive tokens.  Needs
@@ -749,16 +842,26 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
       st_cb = kk - st_tap * gcin;
     }
   }
-  // Issue the loads of K tile kt into stage `stg` (tiles are issued in order).
-  auto issue = [&](int kt, int stg) {
+  // The segment fields the refills read, read once as values (selected
+  // per tile rather than re-read from the kernel arguments: the scalar
+  // loads of a re-read stall the large tiles' loop on their waits).
+  const void *g0s0 = a.seg[0].src0, *g0s1 = a.seg[0].src1, *g1s0 = a.seg[1].src0, *g1s1 = a.seg[1].src1;
+  const int g0cin = a.seg[0].cin, g0ks = a.seg[0].ks, g0c0 = a.seg[0].c0, g0c1 = a.seg[0].c1, g0py = a.seg[0].py,
+            g0px = a.seg[0].px, g0K = a.seg[0].K, gM = a.M;
+  const int g1cin = a.seg[1].cin, g1ks = a.seg[1].ks, g1c0 = a.seg[1].c0, g1c1 = a.seg[1].c1, g1py = a.seg[1].py,
+            g1px = a.seg[1].px;
+  // Issue the loads of K tile kt into stage `stg` (tiles are issued in
+  // order).  `live` false: every offset out of range (zeros, no memory
+  // access), for the large tiles' refills past the last tile.
+  auto issue = [&](int kt, int stg, bool live = true) {
     (void)kt;
     const bool s1 = MODE == 1 && st_seg;
-    const int gcin = s1 ? a.seg[1].cin : a.seg[0].cin, gks = s1 ? a.seg[1].ks : a.seg[0].ks;
-    const int gc0 = s1 ? a.seg[1].c0 : a.seg[0].c0, gc1 = s1 ? a.seg[1].c1 : a.seg[0].c1;
-    const void* gs0 = s1 ? a.seg[1].src0 : a.seg[0].src0;
-    const void* gs1 = s1 ? a.seg[1].src1 : a.seg[0].src1;
+    const int gcin = s1 ? g1cin : g0cin, gks = s1 ? g1ks : g0ks;
+    const int gc0 = s1 ? g1c0 : g0c0, gc1 = s1 ? g1c1 : g0c1;
+    const void* gs0 = s1 ? g1s0 : g0s0;
+    const void* gs1 = s1 ? g1s1 : g0s1;
     const int tap = st_tap, cb = st_cb;
-    const int k0 = (s1 ? a.seg[0].K : 0) + tap * gcin + cb;  // the tile's weight columns
+    const int k0 = (s1 ? g0K : 0) + tap * gcin + cb;  // the tile's weight columns
     if constexpr (tapin) {
       if (++st_tap == gks * gks) {
         st_tap = 0;
@@ -782,18 +885,21 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
     const int cs = in0 ? gc0 : gc1, cbase = 2 * (in0 ? cb : cb - gc0);
     bf16* adst = As + stg * BM * DK;
     if constexpr (MODE == 1) {
-      const __amdgpu_buffer_rsrc_t ares = make_rsrc(in0 ? gs0 : gs1, (long)a.M * cs * 2);
+      const __amdgpu_buffer_rsrc_t ares = make_rsrc(in0 ? gs0 : gs1, (long)gM * cs * 2);
       // tap offset (dy, dx) and its bit in the 3x3 in-image mask (a 1x1 tap
       // is the centre; an upsample phase's 2x2 taps are four of the nine)
-      const int gpy = s1 ? a.seg[1].py : a.seg[0].py, gpx = s1 ? a.seg[1].px : a.seg[0].px;
-      const int tdy = gks == 3 ? tap / 3 - 1 : (gks == 2 ? gpy - 1 + (tap >> 1) : 0);
-      const int tdx = gks == 3 ? tap % 3 - 1 : (gks == 2 ? gpx - 1 + (tap & 1) : 0);
+      const int gpy = s1 ? g1py : g0py, gpx = s1 ? g1px : g0px;
+      // (arithmetic rather than selects, so the refill has no branch: a
+      // masked element gets bit 31 set, beyond every source's size)
+      const int t3 = tap / 3, is3 = gks == 3, is2 = gks == 2;
+      const int tdy = is3 * (t3 - 1) + is2 * (gpy - 1 + (tap >> 1));
+      const int tdx = is3 * (tap - 3 * t3 - 1) + is2 * (gpx - 1 + (tap & 1));
       const int t9 = (tdy + 1) * 3 + tdx + 1;
       const int dpix = tdy * Wo + tdx;
+      const int dead = (int)!live << 31;
 #pragma unroll
       for (int j = 0; j < AW; ++j) {
-        const bool ok = (ra1[j] >> t9) & 1;
-        const int off = ok ? (ra0[j] + dpix) * cs * 2 + cbase + achunk[j] * 16 : OOB;
+        const int off = ((ra0[j] + dpix) * cs * 2 + cbase + achunk[j] * 16) | (~(ra1[j] >> t9) << 31) | dead;
         dma16(ares, adst + (wave * AW + j) * 512, off);
       }
     } else {
@@ -817,7 +923,7 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
           ix = ox * g.stride + kx;
           ok = iy >= 0 && iy < g.Hi && ix >= 0 && ix < g.Wi;
         }
-        ok = ok && ra1[j] >= 0;
+        ok = ok && ra1[j] >= 0 && live;
         const int off = ok ? (ra0[j] + iy * g.Wi + ix) * cs * 2 + cbase + achunk[j] * 16 : OOB;
         dma16(ares, adst + (wave * AW + j) * 512, off);
       }
@@ -826,8 +932,8 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
 #pragma unroll
     for (int j = 0; j < BW; ++j) {
       const int i = wave + NWV * j;
-      if (i < BI)  // wave-uniform
-        dma16(bres, bdst + i * 512, boff[j] == OOB ? OOB : boff[j] + 2 * k0);
+      if (BI % NWV == 0 || i < BI)  // wave-uniform (an OOB row stays beyond the end)
+        dma16(bres, bdst + i * 512, (boff[j] + 2 * k0) | ((int)!live << 31));
     }
   };
 
@@ -840,29 +946,23 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int nk = ke - kb;
-#pragma unroll
-  for (int p = 0; p < DNS - 1; ++p)
-    if (p < nk) issue(kb + p, p);
   const int lr = lane & 31, lh = lane >> 5;
   const int arow = wm * (BM / WM) + lr, brow = wn * (BN / WN) + lr;
-  for (int kt = 0; kt < nk; ++kt) {
-    // Tile kt must have landed; the tiles issued after it may still be in
-    // flight (at most DNS-2 of them, fewer near the end of K).
-    const int ahead = min(DNS - 2, nk - 1 - kt);
-    if (ahead >= 2)
-      wait_vmcnt<2 * LPT_MIN>();
-    else if (ahead == 1)
-      wait_vmcnt<LPT_MIN>();
-    else
-      wait_vmcnt<0>();
-    stage_barrier();
-    if (kt + DNS - 1 < nk) issue(kb + kt + DNS - 1, (kt + DNS - 1) % DNS);
-    const bf16* Ab = As + (kt % DNS) * BM * DK;
-    const bf16* Bb = Bs + (kt % DNS) * BN * DK;
-#pragma unroll
-    for (int ks = 0; ks < DK / 16; ++ks) {
+  if constexpr (TM * TN > 10) {
+    // Large wave tiles run one wave per SIMD, so nothing else hides the
+    // K-step barrier or the fragment reads: the loop is software-pipelined.
+    // All DNS stages are in flight; the fragments of substep ks + 1 are
+    // read before the products of substep ks, and the first fragments of
+    // tile kt + 1 (after its wait and the barrier) before the last products
+    // of tile kt.  Tile kt + DNS refills the stage of tile kt once every
+    // wave has passed that barrier (its reads of tile kt have completed).
+    constexpr int KS = DK / 16;
+    static_assert(KS % 2 == 0, "fragment sets alternate per substep");
+    bf16x8 fa[2][TM], fb[2][TN];
+    auto readf = [&](int stg, int ks, bf16x8 (&af)[TM], bf16x8 (&bfr)[TN]) {
+      const bf16* Ab = As + stg * BM * DK;
+      const bf16* Bb = Bs + stg * BN * DK;
       const int ch = 2 * ks + lh;
-      bf16x8 af[TM], bfr[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int r = arow + i * 32;
@@ -873,11 +973,121 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
         const int r = brow + j * 32;
         bfr[j] = *reinterpret_cast<const bf16x8*>(&Bb[r * DK + 8 * (ch ^ swz<CPR>(r))]);
       }
+    };
+    // Every stage refill is issued, past the last tile as an all-out-of-range
+    // load (zeros into a stage no product reads), so the loop body has no
+    // branch and every wait counts the same DNS - 2 tiles in flight.
+    static_assert(AI % NWV == 0 && BI % NWV == 0, "every wave issues the same loads");
+#pragma unroll
+    for (int p = 0; p < DNS; ++p) issue(kb + p, p, p < nk);
+    wait_vmcnt<(DNS - 1) * LPT_MIN>();  // tile 0 has landed
+    stage_barrier();
+    readf(0, 0, fa[0], fb[0]);
+    auto products = [&](int cur) {
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cur][j], fa[cur][i], acc[i][j], 0, 0, 0);
+    };
+    // The kernel arguments are loaded here, before the wait below (left to
+    // the compiler, some load lazily and are still in flight at the loop;
+    // scalar loads return out of order, so every wait for an LDS read in
+    // the loop would then wait for all of them).  After it the loop's LDS
+    // reads are counted in order: a product waits only for its own
+    // fragments.
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      const ASeg& sg = a.seg[g];
+      asm volatile("" ::"s"(sg.src0), "s"(sg.src1), "s"(sg.cin), "s"(sg.ks), "s"(sg.c0), "s"(sg.c1));
+      asm volatile("" ::"s"(sg.K), "s"(sg.py), "s"(sg.px), "s"(sg.Hi), "s"(sg.Wi), "s"(sg.stride), "s"(sg.up));
+    }
+    {
+      const Epi& e = a.epi;
+      asm volatile("" ::"s"(e.bias), "s"(e.tbias), "s"(e.tb_ld), "s"(e.tb_off), "s"(e.hw), "s"(e.resid), "s"(e.ldr));
+      asm volatile("" ::"s"(e.out), "s"(e.ldo), "s"(e.geglu), "s"(e.qcols), "s"(e.qscale), "s"(e.phase));
+      asm volatile("" ::"s"(e.ph_h), "s"(e.ph_w), "s"(e.rowscale), "s"(a.M), "s"(a.N), "s"(e.out_f32));
+    }
+    wait_lgkm0();
+    __builtin_amdgcn_sched_barrier(0);
+    // every tile but the last: the last substep reads the next tile
+    for (int kt = 0; kt + 1 < nk; ++kt) {
+      static_for<0, KS>([&](auto KSI) {
+        constexpr int ks = KSI.value, cur = ks & 1, nxt = cur ^ 1;
+        if constexpr (ks + 1 < KS) {
+          readf(kt % DNS, ks + 1, fa[nxt], fb[nxt]);
+          __builtin_amdgcn_sched_barrier(0);  // the reads go out before the products
+          products(cur);
+        } else {
+          __builtin_amdgcn_sched_barrier(0);  // the previous substep's products stay above
+          // tiles issued after kt + 1: kt + 2 .. kt + DNS - 1
+          wait_vmcnt<(DNS - 2) * LPT_MIN>();
+          wait_lgkm0();  // this wave's reads of tile kt are complete
+          stage_barrier();
+          __builtin_amdgcn_sched_barrier(0);
+          readf((kt + 1) % DNS, 0, fa[nxt], fb[nxt]);
+          issue(kb + kt + DNS, kt % DNS, kt + DNS < nk);
+          products(cur);
+          // each fragment read, then each refill load, beside a product
+#pragma unroll
+          for (int q = 0; q < TM + TN; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+          }
+#pragma unroll
+          for (int q = 0; q < AW + BW; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+          }
+        }
+      });
+    }
+    if (nk > 0) {
+      static_for<0, KS>([&](auto KSI) {  // the last tile
+        constexpr int ks = KSI.value, cur = ks & 1, nxt = cur ^ 1;
+        if constexpr (ks + 1 < KS) readf((nk - 1) % DNS, ks + 1, fa[nxt], fb[nxt]);
+        products(cur);
+      });
+    }
+    wait_vmcnt<0>();  // the refills past the last tile have landed
+  } else {
+#pragma unroll
+    for (int p = 0; p < DNS - 1; ++p)
+      if (p < nk) issue(kb + p, p);
+    for (int kt = 0; kt < nk; ++kt) {
+      // Tile kt must have landed; the tiles issued after it may still be in
+      // flight (at most DNS-2 of them, fewer near the end of K).
+      const int ahead = min(DNS - 2, nk - 1 - kt);
+      if (ahead >= 2)
+        wait_vmcnt<2 * LPT_MIN>();
+      else if (ahead == 1)
+        wait_vmcnt<LPT_MIN>();
+      else
+        wait_vmcnt<0>();
+      stage_barrier();
+      if (kt + DNS - 1 < nk) issue(kb + kt + DNS - 1, (kt + DNS - 1) % DNS);
+      const bf16* Ab = As + (kt % DNS) * BM * DK;
+      const bf16* Bb = Bs + (kt % DNS) * BN * DK;
+#pragma unroll
+      for (int ks = 0; ks < DK / 16; ++ks) {
+        const int ch = 2 * ks + lh;
+        bf16x8 af[TM], bfr[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int r = arow + i * 32;
+          af[i] = *reinterpret_cast<const bf16x8*>(&Ab[r * DK + 8 * (ch ^ swz<CPR>(r))]);
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int r = brow + j * 32;
+          bfr[j] = *reinterpret_cast<const bf16x8*>(&Bb[r * DK + 8 * (ch ^ swz<CPR>(r))]);
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+      }
     }
   }
   if (a.ksplit > 1) {
@@ -902,18 +1112,28 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
     });
     return;
   }
-  static_assert(32 * (BN / WN) <= 32 * STAGED_LD<BN / WN>, "transposed staging fits the region");
-  const bool vt_ok = a.epi.vt_out && a.epi.vt_col0 % (BN / WN) == 0 && a.epi.vt_hw % 32 == 0 && a.epi.vt_ld % 8 == 0;
-  if ((!a.epi.vt_out || vt_ok) && !a.epi.out_f32 && (!a.epi.resid || !a.epi.geglu)) {
+  if constexpr (TM * TN > 10) {
+    // large wave tiles: the host sends only layers this epilogue covers
+    // (no transposed part, no fp32 output, no residual with GEGLU)
+    static_assert(NWV * 32 * SLAB_LD<BN / WN> * 4 <= (int)sizeof(smem), "slabs fit the operand stages");
     __syncthreads();  // every wave is done with the operand stages
-    bf16* R = smem + wave * 32 * STAGED_LD<BN / WN>;
-    if (a.epi.vt_out && n0 + wn * (BN / WN) >= a.epi.vt_col0)
-      epilogue_staged_vt<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane, R);
-    else
-      epilogue_staged<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane, R);
+    epilogue_slab<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane,
+                                  reinterpret_cast<float*>(smem) + wave * 32 * SLAB_LD<BN / WN>);
     return;
+  } else {
+    static_assert(32 * (BN / WN) <= 32 * STAGED_LD<BN / WN>, "transposed staging fits the region");
+    const bool vt_ok = a.epi.vt_out && a.epi.vt_col0 % (BN / WN) == 0 && a.epi.vt_hw % 32 == 0 && a.epi.vt_ld % 8 == 0;
+    if ((!a.epi.vt_out || vt_ok) && !a.epi.out_f32 && (!a.epi.resid || !a.epi.geglu)) {
+      __syncthreads();  // every wave is done with the operand stages
+      bf16* R = smem + wave * 32 * STAGED_LD<BN / WN>;
+      if (a.epi.vt_out && n0 + wn * (BN / WN) >= a.epi.vt_col0)
+        epilogue_staged_vt<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane, R);
+      else
+        epilogue_staged<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane, R);
+      return;
+    }
+    epilogue_tiles<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane);
   }
-  epilogue_tiles<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane);
 }
 
 // Sum of the split-K partials in split order, then the epilogue.
@@ -1109,7 +1329,21 @@ hipError_t launch_gemm(DType dt, const GemmArgs& args, hipStream_t s) {
   if (dt == BF16) {
     auto nblk = [&](int bm, int bn) { return (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn); };
     const long want = 2 * 256;
-    if (a.N % 160 == 0) {
+    // Long-K layers of widths that are multiples of 256 (the 1280-wide
+    // levels) may take 256x256 tiles: four waves of 128x128 with the
+    // accumulators in AGPRs, one block per CU (3 x 32 KB stages), about 14 %
+    // faster per tile-product than two 256x160 blocks per CU.  With one
+    // block per CU the last wave of blocks can leave much of the chip idle,
+    // so they are taken only where their share of busy block slots, with
+    // that margin, is at least the narrower tiles' (two per CU).  Every
+    // tile gives the same bits, so the choice may follow the row count.
+    auto busy = [](long blocks, long slots) { return (double)blocks / (double)(((blocks + slots - 1) / slots) * slots); };
+    const long n_wide = nblk(256, 256) * a.ksplit;
+    const long n_alt = (a.N % 160 == 0 ? nblk(256, 160) : nblk(256, 128)) * a.ksplit;
+    if (a.N % 256 == 0 && a.K >= 2560 && n_wide >= 128 && 1.1 * busy(n_wide, 256) >= busy(n_alt, 512) &&
+        loader_mode(a, DKS) == 1 && !a.epi.vt_out && !a.epi.out_f32 && !(a.epi.resid && a.epi.geglu) &&
+        launch_dma<256, 256, 2, 2, 3, 1>(a, s)) {
+    } else if (a.N % 160 == 0) {
       // 256x160 tiles through the direct-to-LDS pipeline whenever the loader
       // is uniform: taller tiles cut the weight re-reads that dominate
       // small-M layers.  Three K stages (two for the split-K layers) still

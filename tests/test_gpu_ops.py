@@ -370,6 +370,48 @@ def test_conv_large_grid_rows_independent(ops):
     assert np.array_equal(full, part)
 
 
+WIDE_CASES = [
+    # n, H, W, c0, c1, cout, resid, split.  Every case routes the whole batch to
+    # the 256x256 tiles (width % 256, K >= 2560, at least 128 blocks x splits,
+    # uniform-tap loader) and its first three images alone to the 256x160 or
+    # 256x128 tiles (too few blocks).
+    (40, 16, 16, 1280, 0, 1280, True, True),    # split in 2 (16x16 images), 400 blocks
+    (40, 16, 16, 1280, 0, 1280, True, False),   # one pass, 200 blocks
+    (130, 8, 8, 640, 0, 1280, True, True),      # 8x8 images: tap-outer K order, split in 4
+    (113, 12, 12, 1280, 0, 512, False, True),   # ragged last row tile (16272 rows), no split
+    (35, 31, 31, 160, 160, 256, True, True),    # concat sources, K = 2880, ragged (33635 rows)
+]
+
+
+@pytest.mark.parametrize("case", WIDE_CASES)
+def test_conv_wide_tiles(ops, case):
+    """The 256x256 tiles (four 128x128 waves, AGPR accumulators) give every
+    image the same bits as the narrower tiles (its first images run alone on
+    those) and match the oracle on the first and last image."""
+    n, H, W, c0, c1, cout, with_resid, split = case
+    log(f"wide tiles {case}")
+    rng = np.random.default_rng(hash(case) % 2**32)
+    x0 = _vals(rng, (n, H, W, c0), "bf16")
+    x1 = _vals(rng, (n, H, W, c1), "bf16") if c1 else None
+    w = _vals(rng, (cout, c0 + c1, 3, 3), "bf16", 1.0 / math.sqrt(9 * (c0 + c1)))
+    b = rng.standard_normal(cout).astype(np.float32)
+    res = _vals(rng, (n, H, W, cout), "bf16") if with_resid else None
+    wp, bd = _dev(_pack(w), "bf16"), _dev(b)
+
+    def run(k):
+        return ops.conv(_dev(x0[:k], "bf16"), wp, cout, x1=_dev(x1[:k], "bf16") if c1 else None, bias=bd,
+                        resid=_dev(res[:k], "bf16") if with_resid else None, split=split).float().cpu().numpy()
+
+    full, part = run(n), run(3)
+    torch.cuda.synchronize()
+    assert np.array_equal(full[:3], part)
+    for i in (0, n - 1):
+        a = x0[i].astype(np.float64) if not c1 else np.concatenate([x0[i], x1[i]], axis=2).astype(np.float64)
+        ref = O.conv2d(a, w, b, 1) + (res[i] if with_resid else 0)
+        err = rel_l2(full[i], ref)
+        assert err <= TOL["bf16"], (i, err)
+
+
 OUT_CASES = [
     # n_req, cfg flags, H, W, C, in place, eps_out
     (3, (1, 0, 1), 12, 10, 64, False, True),     # one ragged tile (120 pixels)
