@@ -394,9 +394,11 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& a, const f32x16 
 // Epilogue of the large wave tiles (128 x 128 per wave, accumulators in
 // AGPRs): each 32-row group of the wave is first written raw (fp32) into a
 // wave-private LDS slab, then finished from there in row-contiguous runs of
-// 8 outputs per lane (bias, time bias, row scale, residual, query scale or
-// GEGLU), with the same arithmetic as the other epilogues.  Reading the
-// accumulators only to copy them keeps the register demand low.
+// 8 outputs per lane (bias, time bias, residual), with the same arithmetic
+// as the other epilogues.  Reading the accumulators only to copy them keeps
+// the register demand low (the register-staged epilogue spilled here).
+// The host sends only layers without GEGLU, a row scale, query columns, a
+// transposed part or an fp32 output.
 template <int WC>
 constexpr int SLAB_LD = WC + 4;  // floats per slab row
 
@@ -405,13 +407,12 @@ __device__ __forceinline__ void epilogue_slab(const GemmArgs& a, const f32x16 (&
                                               int wm, int wn, int lane, float* R) {
   constexpr int WC = BN / WN;
   constexpr int LD = SLAB_LD<WC>;
+  constexpr int CP = WC / 8, NCH = 32 * CP / 64;  // 8-output chunks per row; per lane
+  static_assert((32 * CP) % 64 == 0, "row chunks spread evenly over the lanes");
   const Epi& e = a.epi;
-  const bool geglu = e.geglu;
   const int lr = lane & 31, hq = 4 * (lane >> 5);
-  const int nc0 = n0 + wn * WC;                                // first accumulator column of the wave
-  const int ncol0 = geglu ? nc0 / 2 : nc0;                     // first output column
-  const int nout = geglu ? a.N / 2 : a.N;
-  const bf16* resid = reinterpret_cast<const bf16*>(e.resid);  // (never with GEGLU)
+  const int nc0 = n0 + wn * WC;  // first column of the wave
+  const bf16* resid = reinterpret_cast<const bf16*>(e.resid);
   static_for<0, TM>([&](auto I) {
     const int mrow0 = m0 + wm * (BM / WM) + I.value * 32;
     static_for<0, TN>([&](auto J) {
@@ -422,64 +423,40 @@ __device__ __forceinline__ void epilogue_slab(const GemmArgs& a, const f32x16 (&
             make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
     });
     asm volatile("" ::: "memory");  // (one wave's LDS accesses complete in order)
-    auto finish = [&](auto cpc) {
-      constexpr int CP = decltype(cpc)::value, NCH = 32 * CP / 64;  // output chunks per row, per lane
-      static_assert((32 * CP) % 64 == 0, "row chunks spread evenly over the lanes");
-      bf16x8 rr[NCH];
-      if (resid) {
-#pragma unroll
-        for (int u = 0; u < NCH; ++u) {
-          const int c = lane + 64 * u, row = c / CP, ch = c - row * CP, m = mrow0 + row;
-          bf16x8 r = {};
-          if (m < a.M) r = *reinterpret_cast<const bf16x8*>(resid + (long)m * e.ldr + ncol0 + ch * 8);
-          rr[u] = r;
-        }
-      }
+    bf16x8 rr[NCH];
+    if (resid) {
 #pragma unroll
       for (int u = 0; u < NCH; ++u) {
         const int c = lane + 64 * u, row = c / CP, ch = c - row * CP, m = mrow0 + row;
-        const float rs = row_scale(e, m, a.M);
-        float x[8];
-        if (geglu) {
-          // output chunk ch: value columns 32 t + 8 h + [0, 8), gate 16 further
-          const int col = (ch >> 1) * 32 + 8 * (ch & 1);
-          const float* src = R + row * LD + col;
-#pragma unroll
-          for (int k = 0; k < 8; ++k) {
-            const float ba = e.bias ? e.bias[nc0 + col + k] : 0.f, bg = e.bias ? e.bias[nc0 + col + 16 + k] : 0.f;
-            const float av = fmaf(src[k], rs, ba);
-            const float g = fmaf(src[16 + k], rs, bg);
-            x[k] = av * gelu_as(g);
-          }
-        } else {
-          const int col = 8 * ch, n = nc0 + col;
-          const float* src = R + row * LD + col;
-#pragma unroll
-          for (int k = 0; k < 8; ++k) x[k] = fmaf(src[k], rs, e.bias ? e.bias[n + k] : 0.f);
-          if (e.tbias && m < a.M) {
-            const float* tb = e.tbias + (long)(m / e.hw) * e.tb_ld + e.tb_off + n;
-#pragma unroll
-            for (int k = 0; k < 8; ++k) x[k] += tb[k];
-          }
-          if (resid) {
-#pragma unroll
-            for (int k = 0; k < 8; ++k) x[k] += (float)rr[u][k];
-          }
-#pragma unroll
-          for (int k = 0; k < 8; ++k)
-            if (n + k < e.qcols) x[k] *= e.qscale;
-        }
-        bf16x8 o;
-#pragma unroll
-        for (int k = 0; k < 8; ++k) o[k] = (bf16)x[k];
-        if (m < a.M && ncol0 + ch * 8 < nout)
-          *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(e.out) + out_row(e, m) * e.ldo + ncol0 + ch * 8) = o;
+        bf16x8 r = {};
+        if (m < a.M) r = *reinterpret_cast<const bf16x8*>(resid + (long)m * e.ldr + nc0 + ch * 8);
+        rr[u] = r;
       }
-    };
-    if (geglu)
-      finish(IC<WC / 16>{});
-    else
-      finish(IC<WC / 8>{});
+    }
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) {
+      const int c = lane + 64 * u, row = c / CP, ch = c - row * CP, m = mrow0 + row;
+      const int n = nc0 + 8 * ch;
+      const float* src = R + row * LD + 8 * ch;
+      // (one rounding for the bias: fmaf with scale 1, as in the other epilogues)
+      float x[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) x[k] = fmaf(src[k], 1.0f, e.bias ? e.bias[n + k] : 0.f);
+      if (e.tbias && m < a.M) {
+        const float* tb = e.tbias + (long)(m / e.hw) * e.tb_ld + e.tb_off + n;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) x[k] += tb[k];
+      }
+      if (resid) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) x[k] += (float)rr[u][k];
+      }
+      bf16x8 o;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) o[k] = (bf16)x[k];
+      if (m < a.M)
+        *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(e.out) + out_row(e, m) * e.ldo + n) = o;
+    }
     asm volatile("" ::: "memory");
   });
 }
@@ -1114,7 +1091,6 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void gemm_bf16_dma_kernel(GemmA
   }
   if constexpr (TM * TN > 10) {
     // large wave tiles: the host sends only layers this epilogue covers
-    // (no transposed part, no fp32 output, no residual with GEGLU)
     static_assert(NWV * 32 * SLAB_LD<BN / WN> * 4 <= (int)sizeof(smem), "slabs fit the operand stages");
     __syncthreads();  // every wave is done with the operand stages
     epilogue_slab<BM, BN, WM, WN>(a, acc, m0, n0, wm, wn, lane,
@@ -1341,8 +1317,8 @@ hipError_t launch_gemm(DType dt, const GemmArgs& args, hipStream_t s) {
     const long n_wide = nblk(256, 256) * a.ksplit;
     const long n_alt = (a.N % 160 == 0 ? nblk(256, 160) : nblk(256, 128)) * a.ksplit;
     if (a.N % 256 == 0 && a.K >= 2560 && n_wide >= 128 && 1.1 * busy(n_wide, 256) >= busy(n_alt, 512) &&
-        loader_mode(a, DKS) == 1 && !a.epi.vt_out && !a.epi.out_f32 && !(a.epi.resid && a.epi.geglu) &&
-        launch_dma<256, 256, 2, 2, 3, 1>(a, s)) {
+        loader_mode(a, DKS) == 1 && !a.epi.vt_out && !a.epi.out_f32 && !a.epi.geglu && !a.epi.rowscale &&
+        a.epi.qcols == 0 && launch_dma<256, 256, 2, 2, 3, 1>(a, s)) {
     } else if (a.N % 160 == 0) {
       // 256x160 tiles through the direct-to-LDS pipeline whenever the loader
       // is uniform: taller tiles cut the weight re-reads that dominate
