@@ -1236,10 +1236,10 @@ static void launch_bf16(const GemmArgs& a, hipStream_t s) {
 
 // Direct-to-LDS kernel for the uniform-tap modes; false if the layer needs
 // the register-staged loader.
-template <int BM, int BN, int WM, int WN, int DNS, int MINB, int DK = DKS>
+template <int BM, int BN, int WM, int WN, int DNS, int MINB, int DK = DKS, bool UNIFORM_ONLY = false>
 static bool launch_dma(const GemmArgs& a, hipStream_t s) {
   const int mode = loader_mode(a, DK);
-  if (mode == 0 || (DK != DKS && a.ksplit > 1)) return false;
+  if (mode == 0 || (UNIFORM_ONLY && mode != 1) || (DK != DKS && a.ksplit > 1)) return false;
   const long blocks = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN) * a.ksplit;
   const dim3 g((unsigned)blocks), b(64 * WM * WN);
   // K order (see the kernel): channel block outer, taps inner on images
@@ -1249,10 +1249,12 @@ static bool launch_dma(const GemmArgs& a, hipStream_t s) {
     gemm_bf16_dma_kernel<BM, BN, WM, WN, 1, DNS, MINB, DK, true><<<g, b, 0, s>>>(a);
   else if (mode == 1)
     gemm_bf16_dma_kernel<BM, BN, WM, WN, 1, DNS, MINB, DK, false><<<g, b, 0, s>>>(a);
-  else if (ti)
-    gemm_bf16_dma_kernel<BM, BN, WM, WN, 2, DNS, MINB, DK, true><<<g, b, 0, s>>>(a);
-  else
-    gemm_bf16_dma_kernel<BM, BN, WM, WN, 2, DNS, MINB, DK, false><<<g, b, 0, s>>>(a);
+  else if constexpr (!UNIFORM_ONLY) {
+    if (ti)
+      gemm_bf16_dma_kernel<BM, BN, WM, WN, 2, DNS, MINB, DK, true><<<g, b, 0, s>>>(a);
+    else
+      gemm_bf16_dma_kernel<BM, BN, WM, WN, 2, DNS, MINB, DK, false><<<g, b, 0, s>>>(a);
+  }
   if (a.ksplit > 1) {
     const long n = (long)a.M * (a.N / 4);
     splitk_reduce_kernel<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s>>>(a);
@@ -1317,8 +1319,8 @@ hipError_t launch_gemm(DType dt, const GemmArgs& args, hipStream_t s) {
     const long n_wide = nblk(256, 256) * a.ksplit;
     const long n_alt = (a.N % 160 == 0 ? nblk(256, 160) : nblk(256, 128)) * a.ksplit;
     if (a.N % 256 == 0 && a.K >= 2560 && n_wide >= 128 && 1.1 * busy(n_wide, 256) >= busy(n_alt, 512) &&
-        loader_mode(a, DKS) == 1 && !a.epi.vt_out && !a.epi.out_f32 && !a.epi.geglu && !a.epi.rowscale &&
-        a.epi.qcols == 0 && launch_dma<256, 256, 2, 2, 3, 1>(a, s)) {
+        !a.epi.vt_out && !a.epi.out_f32 && !a.epi.geglu && !a.epi.rowscale && a.epi.qcols == 0 &&
+        launch_dma<256, 256, 2, 2, 3, 1, DKS, true>(a, s)) {
     } else if (a.N % 160 == 0) {
       // 256x160 tiles through the direct-to-LDS pipeline whenever the loader
       // is uniform: taller tiles cut the weight re-reads that dominate
