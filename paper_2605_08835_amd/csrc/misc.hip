@@ -651,6 +651,54 @@ __global__ __launch_bounds__(256) void layernorm_rstd_kernel(const T* x, float* 
   }
 }
 
+// The same scale with L lanes per token (64 / L tokens per wave), each lane
+// holding NV vectors of 8 (C = 8 L NV): every lane loads, and a token's
+// sums take log2(L) exchanges within its lane group.  Used where C / 8
+// splits evenly (C = 320, 640, 1280, ...), so that no lane idles as with a
+// wave per token at C = 320.
+template <typename T, int L, int NV>
+__global__ __launch_bounds__(256) void layernorm_rstd_grp_kernel(const T* x, float* rstd, long tokens, float eps) {
+  constexpr int C = 8 * L * NV;
+  const int lane = threadIdx.x & 63, g = lane % L;
+  const long t = ((long)blockIdx.x * 4 + (threadIdx.x >> 6)) * (64 / L) + lane / L;
+  float v[NV][8];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    if (t < tokens) {
+      load8f(x + t * C + (g + L * j) * 8, v[j]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[j][i] = 0.f;
+    }
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < NV; ++j)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s += v[j][i];
+#pragma unroll
+  for (int o = L / 2; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+  const float mean = s / C;
+  float q = 0.f;
+#pragma unroll
+  for (int j = 0; j < NV; ++j)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float d = v[j][i] - mean;
+      q = fmaf(d, d, q);
+    }
+#pragma unroll
+  for (int o = L / 2; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
+  if (g == 0 && t < tokens) rstd[t] = rsqrtf(q / C + eps);
+}
+
+template <typename T, int L, int NV>
+static void launch_ln_rstd_grp(const void* x, float* rstd, long tokens, float eps, hipStream_t s) {
+  constexpr long TPB = 4 * (64 / L);  // tokens per block
+  const unsigned blocks = (unsigned)((tokens + TPB - 1) / TPB);
+  layernorm_rstd_grp_kernel<T, L, NV><<<blocks, 256, 0, s>>>((const T*)x, rstd, tokens, eps);
+}
+
 template <typename T, int MV, int U>
 static void launch_ln_rstd(const void* x, float* rstd, long tokens, int C, float eps, hipStream_t s) {
   const unsigned blocks = (unsigned)((tokens + 4 * U - 1) / (4 * U));
@@ -661,6 +709,12 @@ static void launch_ln_rstd(const void* x, float* rstd, long tokens, int C, float
 // per wave for C <= 512, 2 above (4 loads per lane in flight at C = 640).
 template <typename T>
 static void launch_ln_rstd_t(const void* x, float* rstd, long tokens, int C, float eps, hipStream_t s) {
+  switch (C) {  // the SD / SDXL widths: lane groups of five vectors per lane
+    case 320: launch_ln_rstd_grp<T, 8, 5>(x, rstd, tokens, eps, s); return;
+    case 640: launch_ln_rstd_grp<T, 16, 5>(x, rstd, tokens, eps, s); return;
+    case 1280: launch_ln_rstd_grp<T, 32, 5>(x, rstd, tokens, eps, s); return;
+    default: break;
+  }
   switch ((C / 8 + 63) / 64) {
     case 1: launch_ln_rstd<T, 1, 4>(x, rstd, tokens, C, eps, s); break;
     case 2: launch_ln_rstd<T, 2, 2>(x, rstd, tokens, C, eps, s); break;
