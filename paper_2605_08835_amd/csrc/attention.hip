@@ -79,36 +79,37 @@ __device__ __forceinline__ void static_for(F&& f) {
 
 __device__ inline bf16x8 ld16(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
-// Online-softmax step on one 64-key tile of S^T.  On entry s holds the raw
+// Online-softmax step on one 64-key tile of S^T (NKT = 2), or on its first
+// 32 keys (NKT = 1: a last tile of at most 32 keys).  On entry s holds the raw
 // products: base-2 logits minus m when MF, base-2 logits when QS, plain
 // q.k otherwise.  Moves m where the tile exceeds it by more than TAU,
 // rescales the accumulators then, and leaves P = exp2(logit - m) in s.  SF:
 // the row sum comes out of the PV product, else it is added up here.
-template <int NJ, int ND, bool QS, bool MF, bool SF, bool TAIL>
+template <int NJ, int ND, bool QS, bool MF, bool SF, bool TAIL, int NKT = 2>
 __device__ __forceinline__ void softmax_tile(f32x16 (&s)[2], f32x16 (&o)[ND], bf16x8 (&qf)[NJ], float& m_run,
                                              float& l_run, bool first, int kvalid, int lh, int d, float sl2) {
   using namespace fa;
   if constexpr (!QS) {
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[kt][r] = fmaf(s[kt][r], sl2, -m_run);
   } else if constexpr (!MF) {  // no spare column: subtract m here
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[kt][r] -= m_run;
   }
   if constexpr (TAIL) {  // keys at or past kvalid; compared as immediates against one register
     const int lim = kvalid - 4 * lh;
-    static_for<0, 32>([&](auto I) {
+    static_for<0, 16 * NKT>([&](auto I) {
       constexpr int kt = I.value / 16, r = I.value % 16;
       if (kt * 32 + 8 * (r >> 2) + (r & 3) >= lim) s[kt][r] = -1e30f;
     });
   }
   float mt = -1e30f;
 #pragma unroll
-  for (int kt = 0; kt < 2; ++kt)
+  for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[kt][r]);
   mt = xor32_max(mt);
@@ -125,7 +126,7 @@ __device__ __forceinline__ void softmax_tile(f32x16 (&s)[2], f32x16 (&o)[ND], bf
     // size, so alpha is not evaluated there)
     const float alpha = first ? 0.f : __builtin_amdgcn_exp2f(-delta);
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[kt][r] -= delta;
     l_run *= alpha;
@@ -143,13 +144,13 @@ __device__ __forceinline__ void softmax_tile(f32x16 (&s)[2], f32x16 (&o)[ND], bf
     }
   }
 #pragma unroll
-  for (int kt = 0; kt < 2; ++kt)
+  for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) s[kt][r] = __builtin_amdgcn_exp2f(s[kt][r]);
   if constexpr (!SF) {
     float ps = 0.f;
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) ps += s[kt][r];
     l_run += ps;
@@ -401,9 +402,14 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
   // fk / fv: the set to fetch the tile after next into; sk / sv: the set
   // holding the next tile, staged at the end.
   // FULL: the tile it fetches is full and V^T is aligned (FAST heads only).
+  // HALF (a tail of at most 32 keys): only the first 32-key block of S^T and
+  // the first two PV slices; the keys past it were masked to P = 0, so the
+  // products skipped added exact zeros and the result is the same.
   auto tile = [&](auto tl, auto ff, int k0, int it, bf16x8 (&fk)[KPT], bf16x8 (&fv)[VPT], bf16x8 (&sk)[KPT],
-                  bf16x8 (&sv)[VPT]) {
-    constexpr bool TAIL = decltype(tl)::value, FULL = decltype(ff)::value;
+                  bf16x8 (&sv)[VPT], auto hf) {
+    constexpr bool TAIL = decltype(tl)::value, FULL = decltype(ff)::value, HALF = decltype(hf)::value;
+    static_assert(TAIL || !HALF, "only a tail tile is halved");
+    constexpr int NKT = HALF ? 1 : 2;
     const int b = it & 1;
     const bool more = k0 + KT < a.Nk;
     if constexpr (FULL) {
@@ -425,7 +431,7 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[g][kt][r] = 0.f;
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
         const bf16x8 kf = ld16(&Kb[(kt * 32 + lq) * LDK + 16 * j + 8 * lh]);
@@ -434,12 +440,13 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
       }
 #pragma unroll
     for (int g = 0; g < QG; ++g)
-      softmax_tile<NJ, ND, QS, MF, SF, TAIL>(s[g], o[g], qf[g], m_run[g], l_run[g], it == 0, a.Nk - k0, lh, d, sl2);
+      softmax_tile<NJ, ND, QS, MF, SF, TAIL, NKT>(s[g], o[g], qf[g], m_run[g], l_run[g], it == 0, a.Nk - k0, lh, d,
+                                                  sl2);
 
     // O^T += V^T P^T over four 16-key slices.  Slot (lh, i) of slice u is
     // key 16u + 8(i/4) + 4 lh + i%4, i.e. register 8(u%2) + i of S^T tile u/2.
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < 2 * NKT; ++u) {
       bf16x8 pf[QG];
 #pragma unroll
       for (int g = 0; g < QG; ++g)
@@ -480,24 +487,35 @@ __global__ __launch_bounds__(64 * NW, D16 <= 128 ? 2 : 1) void attn_bf16_kernel(
     // pairs whose fetch targets (tiles it + 2 and it + 3) are both full
     if (full_ok)
       for (; (it + 4) * KT <= a.Nk; it += 2) {
-        tile(BC<false>{}, BC<FAST>{}, it * KT, it, rk0, rv0, rk1, rv1);
-        tile(BC<false>{}, BC<FAST>{}, (it + 1) * KT, it + 1, rk1, rv1, rk0, rv0);
+        tile(BC<false>{}, BC<FAST>{}, it * KT, it, rk0, rv0, rk1, rv1, BC<false>{});
+        tile(BC<false>{}, BC<FAST>{}, (it + 1) * KT, it + 1, rk1, rv1, rk0, rv0, BC<false>{});
       }
     for (; it + 1 < nfull; it += 2) {
-      tile(BC<false>{}, BC<false>{}, it * KT, it, rk0, rv0, rk1, rv1);
-      tile(BC<false>{}, BC<false>{}, (it + 1) * KT, it + 1, rk1, rv1, rk0, rv0);
+      tile(BC<false>{}, BC<false>{}, it * KT, it, rk0, rv0, rk1, rv1, BC<false>{});
+      tile(BC<false>{}, BC<false>{}, (it + 1) * KT, it + 1, rk1, rv1, rk0, rv0, BC<false>{});
     }
     if (it < nfull) {
-      tile(BC<false>{}, BC<false>{}, it * KT, it, rk0, rv0, rk1, rv1);
+      tile(BC<false>{}, BC<false>{}, it * KT, it, rk0, rv0, rk1, rv1, BC<false>{});
       ++it;
     }
   } else {
     if (full_ok)
-      for (; (it + 2) * KT <= a.Nk; ++it) tile(BC<false>{}, BC<FAST>{}, it * KT, it, rk0, rv0, rk0, rv0);
-    for (; it < nfull; ++it) tile(BC<false>{}, BC<false>{}, it * KT, it, rk0, rv0, rk0, rv0);
+      for (; (it + 2) * KT <= a.Nk; ++it) tile(BC<false>{}, BC<FAST>{}, it * KT, it, rk0, rv0, rk0, rv0, BC<false>{});
+    for (; it < nfull; ++it) tile(BC<false>{}, BC<false>{}, it * KT, it, rk0, rv0, rk0, rv0, BC<false>{});
   }
   // (the partial last tile fetches and stages nothing)
-  if (nfull * KT < a.Nk) tile(BC<true>{}, BC<false>{}, nfull * KT, it, rk0, rv0, rk1, rv1);
+  // The half tail is built for the pre-scaled widths of SD-1.5's heads
+  // (d = 40, 80, 160: the 77-token cross-attention's 13-key tail); at the
+  // other widths the second tail instance made the kernel spill.
+  constexpr bool HALF_OK = QS && (D16 == 48 || D16 == 80 || D16 == 160);
+  if constexpr (HALF_OK) {
+    if (nfull * KT + 32 >= a.Nk && nfull * KT < a.Nk)
+      tile(BC<true>{}, BC<false>{}, nfull * KT, it, rk0, rv0, rk1, rv1, BC<true>{});
+    else if (nfull * KT < a.Nk)
+      tile(BC<true>{}, BC<false>{}, nfull * KT, it, rk0, rv0, rk1, rv1, BC<false>{});
+  } else {
+    if (nfull * KT < a.Nk) tile(BC<true>{}, BC<false>{}, nfull * KT, it, rk0, rv0, rk1, rv1, BC<false>{});
+  }
 
   // O^T accumulator: lane holds head dims t*32 + 8(r/4) + 4 lh + [0, 4) of
   // its query; each run of 4 is one 8-byte store.

@@ -181,6 +181,8 @@ def test_upconv_rejects_unsupported_widths(ops):
     # key counts in whole 8-key chunks take the direct-to-LDS tiles (partial last tile, folded max)
     (8, 40, 130, 256, 1.0, False), (2, 24, 100, 64, 30.0, True), (8, 40, 64, 200, 1.0, True),
     (4, 56, 96, 136, 1.0, False), (8, 40, 32, 8, 1.0, True), (2, 64, 70, 520, 30.0, False),
+    # last tiles of at most 32 keys (the half tail at d = 40, 72, 80, 160)
+    (2, 72, 50, 90, 1.0, True), (4, 80, 40, 96, 1.0, True),
 ])
 def test_attention(ops, dt, qmode, heads, d, nq, nk, scale, cross):
     """bf16 takes V transposed (channel-major, padded token stride, as the
