@@ -343,7 +343,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the step shards by request with no collective, "
-              f"and this build runs on a single MI355X (got --gpus {args.gpus}).", file=sys.stderr)
+              f"and each process drives a single MI355X (got --gpus {args.gpus}).", file=sys.stderr)
         sys.exit(2)
 
     import torch
