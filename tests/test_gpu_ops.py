@@ -382,6 +382,7 @@ WIDE_CASES = [
     (130, 8, 8, 640, 0, 1280, True, True),      # 8x8 images: tap-outer K order, split in 4
     (113, 12, 12, 1280, 0, 512, False, True),   # ragged last row tile (16272 rows), no split
     (35, 31, 31, 160, 160, 256, True, True),    # concat sources, K = 2880, ragged (33635 rows)
+    (90, 12, 12, 1280, 0, 1280, True, True),    # split in 2 with a ragged last row tile (12960 rows)
 ]
 
 
