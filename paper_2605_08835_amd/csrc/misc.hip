@@ -18,6 +18,15 @@ __global__ void pack_latents_kernel(const float* lat, T* x0, int rows, int lc, i
   if (i >= (long)rows * hw) return;
   const int row = (int)(i / hw), p = (int)(i - (long)row * hw);
   const int r = row_req[row];
+  if (sizeof(T) == 2 && cpad % 8 == 0) {  // 16-byte runs of 8 channels
+    for (int c0 = 0; c0 < cpad; c0 += 8) {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = c0 + e < lc ? lat[((long)r * lc + c0 + e) * hw + p] : 0.f;
+      store8f(x0 + i * cpad + c0, v);
+    }
+    return;
+  }
   for (int c = 0; c < cpad; ++c) {
     const float v = c < lc ? lat[((long)r * lc + c) * hw + p] : 0.f;
     x0[i * cpad + c] = from_f<T>(v);

@@ -946,6 +946,10 @@ static sd_unet* skeleton(const sd_unet_config* cfg) {
   h->cfg = *cfg;
   h->dt = cfg->dtype == SD_BF16 ? BF16 : F32;
   h->esz = cfg->dtype == SD_BF16 ? 2 : 4;
+  // conv_in's input channels padded to 32 in bf16 (a whole K stage per tap,
+  // so it takes the direct-to-LDS GEMM; the padding adds only zero products),
+  // to 8 in fp32
+  h->cpad = h->dt == BF16 ? 32 : 8;
   h->manifest = build_manifest(*cfg);
   build_layout(h);
   plan_workspace(h);
